@@ -1,0 +1,206 @@
+"""Benchmark of the fused Winograd 3x3 convolution on one MI355X.
+
+A step is one wino_conv_run of the VGG-style layer N=32, C=K=64, 224x224,
+F(4x4,3x3): the kernel transform followed by the fused kernel (input transform,
+per-frequency products on the matrix cores, output transform).  Inputs are
+seeded synthetic tensors already resident in device memory.
+
+The metric is the effective rate, direct-convolution flops (2*N*C*K*H*W*9) per
+second.  The JSON line also carries the fused kernel's own rate against the
+fp32 matrix-core roofline (transform-domain flops 2*T^2*tiles*C*K over the
+kernel's average duration, timed with HIP events on the stream it runs on), the
+three-stage variant's step time on the same layer, and the CPU oracle timed on
+the host cores.
+
+    python bench.py [--steps K] [--warmup W] [--layer ID --m M] [--all] [--no-cpu]
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+P_MFMA_F32 = 157.3e12   # MI355X dense fp32 matrix peak, FLOP/s
+B_HBM = 8.0e12          # MI355X HBM3E peak, B/s
+KERNEL_SRC = os.path.join(ROOT, "paper_1912_02165_amd", "csrc", "wino_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--layer", type=int, default=2)
+    ap.add_argument("--m", type=int, default=4)
+    ap.add_argument("--all", action="store_true", help="also time every (layer, m, algorithm)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--out", default=None, help="append the per-pair table (JSON lines) here")
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were taken
+    on the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            entries = json.load(f)
+    except (OSError, ValueError):
+        return None
+    for e in entries:
+        if (e.get("kernel") == kernel and e.get("workload") == workload
+                and e.get("source_hash") == kernel_source_hash()):
+            return e.get("bytes_per_launch")
+    return None
+
+
+def time_pair(layer, m, algo, steps, warmup, x, w):
+    """Time `steps` steps; returns dict with ms_per_step and the transform-domain
+    kernel's average duration (ms) measured between events on the same stream."""
+    import torch
+    import paper_1912_02165_amd as wc
+    N, C, K, H, W = layer.N, layer.C, layer.K, layer.H, layer.W
+    y = torch.empty((N, K, H, W), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    with wc.Plan(N, C, K, H, W, m, algo) as p:
+        for _ in range(warmup):
+            p.run(x, w, y)
+        torch.cuda.synchronize()
+        # whole steps
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            p.run(x, w, y)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_step = e0.elapsed_time(e1) / steps
+        # the same two phases with an event between them: kernel transform, then the rest
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+                torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        torch.cuda.synchronize()
+        for a, b, c in evs:
+            a.record(stream)
+            p.set_weights(w)
+            b.record(stream)
+            p.run_pretransformed(x, y)
+            c.record(stream)
+        torch.cuda.synchronize()
+        wt_ms = sum(a.elapsed_time(b) for a, b, _ in evs) / steps
+        body_ms = sum(b.elapsed_time(c) for _, b, c in evs) / steps
+        nt, dflops, tflops = p.info()
+    return {"ms_per_step": ms_step, "weight_transform_ms": wt_ms, "body_ms": body_ms,
+            "direct_flops": dflops, "tdomain_flops": tflops, "tiles": nt}
+
+
+def cpu_baseline(layer, budget_s=20.0):
+    """The oracle (plain C direct convolution, fp64 accumulation, OpenMP) on the first
+    images of the layer: one image to size the sample, then as many images as fit in
+    about budget_s seconds (at most the whole layer)."""
+    from paper_1912_02165_amd import workloads
+    from oracle import direct
+    x1, w = workloads.layer_inputs(layer, n_images=1)
+    t = time.perf_counter()
+    direct.direct_conv(x1, w)
+    t1 = time.perf_counter() - t
+    n = max(1, min(layer.N, int(budget_s / max(t1, 1e-3))))
+    if n > 1:
+        xs, w = workloads.layer_inputs(layer, n_images=n)
+        t = time.perf_counter()
+        direct.direct_conv(xs, w)
+        dt = time.perf_counter() - t
+    else:
+        dt = t1
+    flops = layer.direct_flops / layer.N * n
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": direct.num_threads(),
+            "kind": "oracle",
+            "sample": f"{n} of {layer.N} images of {layer.name} (direct conv, fp64 accumulation), "
+                      f"{dt:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the convolution shards over images with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_1912_02165_amd import workloads
+
+    layer = workloads.LAYER_BY_ID[args.layer]
+    m = args.m
+    x_np, w_np = workloads.layer_inputs(layer)
+    x = torch.from_numpy(x_np).cuda()
+    w = torch.from_numpy(w_np).cuda()
+
+    fused = time_pair(layer, m, "fused", args.steps, args.warmup, x, w)
+    three = time_pair(layer, m, "three_stage", args.steps, args.warmup, x, w)
+
+    kernel_ms = fused["body_ms"]
+    achieved = fused["tdomain_flops"] / (kernel_ms * 1e-3)
+    workload = layer.tag(m)
+    traffic = measured_traffic("fused", workload)
+    rec = {
+        "metric": "effective TFLOP/s per conv layer (direct-conv FLOPs) + % of MFMA/HBM roofline",
+        "value": fused["direct_flops"] / (fused["ms_per_step"] * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": fused["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": workload, "N": layer.N, "C": layer.C, "K": layer.K, "H": layer.H,
+                   "W": layer.W, "m": m, "algo": "fused", "stride": 1, "pad": 1},
+        "roofline": {"bound": "mfma", "achieved": achieved / 1e12, "peak": P_MFMA_F32 / 1e12,
+                     "unit": "TFLOP/s", "frac": achieved / P_MFMA_F32, "traffic": traffic,
+                     "kernel": "fused_kernel", "kernel_ms": kernel_ms},
+        "tdomain_tflops_per_step": fused["tdomain_flops"] / (fused["ms_per_step"] * 1e-3) / 1e12,
+        "weight_transform_ms": fused["weight_transform_ms"],
+        "three_stage": {"ms_per_step": three["ms_per_step"],
+                        "value": three["direct_flops"] / (three["ms_per_step"] * 1e-3) / 1e12,
+                        "body_ms": three["body_ms"]},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu:
+        rec["cpu_baseline"] = cpu_baseline(layer)
+
+    if args.all:
+        rows = []
+        for lay, mm in workloads.PAIRS:
+            xn, wn = workloads.layer_inputs(lay)
+            xa, wa = torch.from_numpy(xn).cuda(), torch.from_numpy(wn).cuda()
+            for algo in ("fused", "three_stage"):
+                r = time_pair(lay, mm, algo, args.steps, args.warmup, xa, wa)
+                row = {"workload": lay.tag(mm), "algo": algo, "ms_per_step": r["ms_per_step"],
+                       "eff_tflops": r["direct_flops"] / (r["ms_per_step"] * 1e-3) / 1e12,
+                       "body_ms": r["body_ms"],
+                       "tdomain_tflops_body": r["tdomain_flops"] / (r["body_ms"] * 1e-3) / 1e12,
+                       "mfma_frac_body": r["tdomain_flops"] / (r["body_ms"] * 1e-3) / P_MFMA_F32,
+                       "weight_transform_ms": r["weight_transform_ms"]}
+                rows.append(row)
+                print(json.dumps(row), file=sys.stderr, flush=True)
+            del xa, wa
+        if args.out:
+            with open(args.out, "a") as f:
+                for row in rows:
+                    f.write(json.dumps(row) + "\n")
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,145 @@
+/*
+ * wino_conv.h -- C ABI of a fused Winograd 3x3 convolution for AMD MI355X (gfx950).
+ *
+ * The operation (Sec. 2.1, Eq. 1, with the pad of 1 used in Sec. 6): for every
+ * image n, output channel k and pixel (h, v),
+ *
+ *     y[n,k,h,v] = sum_{c<C} sum_{r<3} sum_{s<3} x[n,c,h+r-1,v+s-1] * w[k,c,r,s]
+ *
+ * with x read as zero outside the image (implicit padding), stride 1.  It is
+ * computed as the Winograd F(m x m, 3 x 3) transformed convolution of Eq. 3,
+ * y = A^T [ sum_c (G w G^T) (.) (B^T d B) ] A over overlap-add tiles of edge
+ * T = m + 2 (Sec. 2.1), for m in {2, 4, 6}.
+ *
+ * Layouts: x is N x C x H x W, w is K x C x 3 x 3, y is N x K x H x W, all dense
+ * row-major fp32.  x, w and y are device pointers on the plan's device.
+ *
+ * Two algorithms compute the same result:
+ *   WINO_ALGO_FUSED       one kernel per call does, for a block of tiles, the
+ *                         input transform, the per-frequency products over C on
+ *                         the matrix cores and the output transform, keeping the
+ *                         transformed tiles on chip (Sec. 4, the "L3 fused" task
+ *                         of R tiles).
+ *   WINO_ALGO_THREE_STAGE the standard pipeline of Sec. 3: all input transforms
+ *                         to device memory, T^2 products over C, then all output
+ *                         transforms.
+ * Both first transform the kernels (Sec. 3, step 2: kernel matrices obtained by
+ * transforming the kernels), unless the weights were set ahead of time with
+ * wino_conv_set_weights.
+ *
+ * Errors: functions return WINO_OK (0) or a negative status; plan constructors
+ * return NULL.  In every failure case wino_last_error() describes it.  Arguments
+ * are checked before any GPU work is queued; the library never aborts, exits or
+ * prints (unless the environment variable WINO_LOG=1, which logs plan choices to
+ * stderr).  Not thread-safe per plan: one plan serves one stream at a time.
+ */
+#ifndef WINO_CONV_H
+#define WINO_CONV_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct wino_plan wino_plan; /* opaque */
+
+enum {
+    WINO_OK = 0,
+    WINO_EINVAL = -1,       /* bad argument */
+    WINO_EUNSUPPORTED = -2, /* valid request this library does not handle */
+    WINO_ENOMEM = -3,       /* device allocation failed */
+    WINO_EHIP = -4          /* a HIP call or kernel launch failed */
+};
+
+enum {
+    WINO_ALGO_FUSED = 0,
+    WINO_ALGO_THREE_STAGE = 1
+};
+
+/* Intermediate buffers a plan owns (for wino_conv_copy_intermediate). */
+enum {
+    WINO_BUF_WEIGHTS = 0,   /* transformed kernels, see wino_conv_intermediate_dims */
+    WINO_BUF_INPUT = 1,     /* three-stage only: transformed input tiles  */
+    WINO_BUF_PRODUCT = 2    /* three-stage only: per-frequency products    */
+};
+
+/* Optional blocking overrides; a field of 0 keeps the automatic choice.
+ *   k_blocks_per_wave: output channels per wave, in blocks of 16 (fused).
+ *   waves_per_group:   waves (of 64 lanes, 16 tiles each) per workgroup (fused). */
+typedef struct {
+    int k_blocks_per_wave;
+    int waves_per_group;
+    int reserved0;
+    int reserved1;
+} wino_tuning;
+
+/* Create a plan for an F(m x m, 3 x 3) convolution of an N x C x H x W input
+ * with K output channels, on the current HIP device, with the fused algorithm
+ * and automatic blocking.  Allocates the plan's device workspace (the
+ * transformed kernels, T^2 * C * K floats rounded up to the blocking).
+ * Returns NULL (see wino_last_error) if a size is < 1, m is not 2, 4 or 6, a
+ * size overflows the 32-bit offsets the kernels use (each of x and y must be
+ * below 2^31 bytes), or the allocation fails. */
+wino_plan *wino_conv_plan(int N, int C, int K, int H, int W, int m);
+
+/* As wino_conv_plan, choosing the algorithm (WINO_ALGO_*) and optional blocking
+ * overrides (t may be NULL).  The three-stage plan also allocates its
+ * intermediate buffers (2 * T^2 * tiles * max(C, K) floats, rounded up). */
+wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
+                             const wino_tuning *t);
+
+/* Queue y = conv(x, w) on stream (a hipStream_t; NULL is the null stream).
+ * Asynchronous: returns once the work is queued; synchronise the stream before
+ * reading y.  y is fully overwritten.  x, w and y must be device allocations on
+ * the plan's device large enough for their tensors, 4-byte aligned, and y must
+ * not overlap x or w.  Returns WINO_EINVAL for a NULL plan or pointer, a bad
+ * pointer, overlap, or a stream of another device; WINO_EHIP if a launch fails. */
+int wino_conv_run(const wino_plan *p, const float *x, const float *w, float *y, void *stream);
+
+/* Steady-state inference (Sec. 3 footnote: kernels transformed ahead of time):
+ * transform w (K x C x 3 x 3, device) into the plan's workspace on stream. */
+int wino_conv_set_weights(wino_plan *p, const float *w, void *stream);
+
+/* Queue y = conv(x, w) with the kernels most recently transformed into the plan
+ * (by wino_conv_set_weights or wino_conv_run), skipping the kernel transform.
+ * Returns WINO_EINVAL if the plan holds no kernels yet, otherwise as wino_conv_run. */
+int wino_conv_run_pretransformed(const wino_plan *p, const float *x, float *y, void *stream);
+
+/* Free the plan and its device memory.  NULL is ignored.  The caller must make
+ * sure no queued work still uses the plan. */
+void wino_conv_destroy(wino_plan *p);
+
+/* Bytes of device workspace the plan holds (0 for NULL). */
+size_t wino_conv_workspace_bytes(const wino_plan *p);
+
+/* Sizes of the problem: number of tiles N*ceil(H/m)*ceil(W/m), direct-convolution
+ * flops 2*N*C*K*H*W*9 and transform-domain flops 2*T^2*tiles*C*K.  Any output
+ * pointer may be NULL.  Returns WINO_EINVAL for a NULL plan. */
+int wino_conv_info(const wino_plan *p, long long *n_tiles, double *direct_flops,
+                   double *tdomain_flops);
+
+/* Logical layout of an intermediate buffer as up to 4 dims (outermost first,
+ * unused trailing dims are 1), for tests that read it back:
+ *   WINO_BUF_WEIGHTS: [Kb][Cs][T^2/4][64][4]: element (f, c, k) of G w[k,c] G^T
+ *                     sits at kb = k/16, cs = c/4, block f/4, lane (c%4)*16 + k%16,
+ *                     slot f%4 (the matrix-core operand order).  Dims returned:
+ *                     {Kb, Cs, T^2, 64} with f in the third dim as described.
+ *   WINO_BUF_INPUT:   [T^2][Cp][tiles_p]  (three-stage plans only)
+ *   WINO_BUF_PRODUCT: [T^2][Kp][tiles_p]  (three-stage plans only)
+ * Frequency f = i*T + j for transform row i, column j; tile t = (n*TH + ty)*TW + tx. */
+int wino_conv_intermediate_dims(const wino_plan *p, int which, long long dims[4]);
+
+/* Copy an intermediate buffer to host memory (count floats, synchronous on the
+ * null stream after a device synchronisation).  Returns WINO_EINVAL if the plan
+ * has no such buffer or count is larger than it. */
+int wino_conv_copy_intermediate(const wino_plan *p, int which, float *host_dst, size_t count);
+
+/* Message describing the last failure on the calling thread ("" if none). */
+const char *wino_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WINO_CONV_H */

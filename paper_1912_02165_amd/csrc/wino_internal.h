@@ -1,0 +1,46 @@
+// Internal declarations shared by the host library (wino_api.cpp) and the
+// kernels (wino_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace wino {
+
+// Problem geometry and device buffers of one plan.
+struct Geometry {
+    int N, C, K, H, W, m;
+    int T, T2;          // input tile edge m + 2 and frequencies T^2
+    int TH, TW;         // tiles per column / row: ceil(H/m), ceil(W/m)
+    int ntiles;         // N * TH * TW
+    int Cs;             // channel steps of 4 (matrix-core reduction depth): ceil(C/4)
+    int Kb;             // output-channel blocks of 16: ceil(K/16)
+    int Kb_alloc;       // Kb rounded up to a multiple of 4 (padding blocks are zero)
+    int tiles_p;        // ntiles rounded up to a multiple of 64 (three-stage buffers)
+};
+
+// Fused-kernel blocking.
+struct FusedCfg {
+    int nkb;    // 16-channel output blocks per wave
+    int waves;  // waves per workgroup (each owns 16 tiles)
+};
+
+// Kernel transform: w (K x C x 3 x 3) -> wt in matrix-core operand order.
+hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt, hipStream_t s);
+
+// Fused: x -> y with the transformed kernels wt.
+hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, const float *wt,
+                        float *y, hipStream_t s);
+
+// Three-stage: x -> U -> M -> y.
+hipError_t launch_input_transform(const Geometry &g, const float *x, float *U, hipStream_t s);
+hipError_t launch_frequency_gemm(const Geometry &g, const float *U, const float *wt, float *M,
+                                 hipStream_t s);
+hipError_t launch_output_transform(const Geometry &g, const float *M, float *y, hipStream_t s);
+
+// Fused blocking the kernels are instantiated for, per m.
+bool fused_cfg_supported(int m, const FusedCfg &cfg);
+FusedCfg fused_cfg_default(const Geometry &g);
+
+}  // namespace wino

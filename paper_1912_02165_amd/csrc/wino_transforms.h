@@ -1,0 +1,242 @@
+// Winograd F(m x m, 3 x 3) transform matrices and their application, for the
+// GPU kernels.
+//
+// The transformed convolution of Sec. 2.1, Eq. 3 needs three matrices the paper
+// does not print: A^T (m x T), G (T x 3) and B^T (T x T), T = m + 2.  They are
+// built here at compile time, in exact rational arithmetic, by the Toom-Cook
+// construction: choose T - 1 finite points p_j plus the point at infinity; then
+//   A^T[i][j] = p_j^i                        (infinity column: [i == m-1])
+//   G[j][u]   = p_j^u / prod_{l!=j}(p_j - p_l) (infinity row: [u == 2])
+//   B^T[j][a] = coefficient of x^a in prod_{l!=j}(x - p_l)
+//               (infinity row: coefficients of prod_l (x - p_l)).
+// Points, in frequency order: F(2): 0, 1, -1; F(4): 0, +-1, +-2;
+// F(6): 0, +-1, +-2, +-1/2.
+//
+// Because the finite points are 0 followed by (+p, -p) pairs, the B^T rows of a
+// pair agree on even coefficients and differ in sign on odd ones, and the A^T
+// columns of a pair differ by (-1)^i.  The 1D transforms below use that to share
+// work between the two rows (even part +- odd part).  Every coefficient is a
+// compile-time constant: zero terms vanish, +-1 become adds and subtracts.
+#pragma once
+
+namespace wino {
+
+// ---- exact rationals, compile time only --------------------------------------
+struct Q {
+    long long n = 0, d = 1;
+};
+
+constexpr long long gcd_ll(long long a, long long b) {
+    a = a < 0 ? -a : a;
+    b = b < 0 ? -b : b;
+    while (b) {
+        long long t = a % b;
+        a = b;
+        b = t;
+    }
+    return a;
+}
+
+constexpr Q mkq(long long n, long long d = 1) {
+    if (d < 0) { n = -n; d = -d; }
+    long long g = gcd_ll(n, d);
+    if (g == 0) g = 1;
+    return Q{n / g, d / g};
+}
+constexpr Q operator+(Q a, Q b) { return mkq(a.n * b.d + b.n * a.d, a.d * b.d); }
+constexpr Q operator-(Q a, Q b) { return mkq(a.n * b.d - b.n * a.d, a.d * b.d); }
+constexpr Q operator*(Q a, Q b) { return mkq(a.n * b.n, a.d * b.d); }
+constexpr Q operator/(Q a, Q b) { return mkq(a.n * b.d, a.d * b.n); }
+constexpr bool operator==(Q a, Q b) { return a.n == b.n && a.d == b.d; }
+constexpr float to_float(Q a) { return (float)((double)a.n / (double)a.d); }
+
+constexpr Q point(int m, int j) {
+    // 0, 1, -1, 2, -2, 1/2, -1/2 (the first m + 1 are used)
+    constexpr long long num[7] = {0, 1, -1, 2, -2, 1, -1};
+    constexpr long long den[7] = {1, 1, 1, 1, 1, 2, 2};
+    return (void)m, mkq(num[j], den[j]);
+}
+
+template <int M>
+struct Tables {
+    static constexpr int T = M + 2;
+    static constexpr int P = T - 1;  // finite points
+    float at[M][T];
+    float g[T][3];
+    float bt[T][T];
+
+    constexpr Tables() : at{}, g{}, bt{} {
+        Q p[P] = {};
+        for (int j = 0; j < P; ++j) p[j] = point(M, j);
+        // A^T
+        for (int i = 0; i < M; ++i) {
+            for (int j = 0; j < P; ++j) {
+                Q v = mkq(1);
+                for (int e = 0; e < i; ++e) v = v * p[j];
+                at[i][j] = to_float(v);
+            }
+            at[i][P] = (i == M - 1) ? 1.0f : 0.0f;
+        }
+        // G
+        for (int j = 0; j < P; ++j) {
+            Q den = mkq(1);
+            for (int l = 0; l < P; ++l)
+                if (l != j) den = den * (p[j] - p[l]);
+            Q pw = mkq(1);
+            for (int u = 0; u < 3; ++u) {
+                g[j][u] = to_float(pw / den);
+                pw = pw * p[j];
+            }
+        }
+        g[P][0] = 0.0f; g[P][1] = 0.0f; g[P][2] = 1.0f;
+        // B^T: row j from prod_{l != j}(x - p_l), row P from prod_l (x - p_l)
+        for (int j = 0; j <= P; ++j) {
+            Q c[T] = {};
+            c[0] = mkq(1);
+            int deg = 0;
+            for (int l = 0; l < P; ++l) {
+                if (l == j) continue;
+                // c(x) *= (x - p_l)
+                for (int e = deg + 1; e >= 1; --e) c[e] = c[e - 1] - c[e] * p[l];
+                c[0] = mkq(0) - c[0] * p[l];
+                ++deg;
+            }
+            for (int a = 0; a < T; ++a) bt[j][a] = to_float(c[a]);
+        }
+    }
+};
+
+template <int M>
+constexpr bool pair_structure_holds() {
+    constexpr Tables<M> tb{};
+    constexpr int T = M + 2;
+    for (int j = 1; j + 1 < T - 1; j += 2) {
+        for (int a = 0; a < T; ++a) {
+            float e = tb.bt[j][a], o = tb.bt[j + 1][a];
+            if (a % 2 == 0 ? (e != o) : (e != -o)) return false;
+        }
+        for (int i = 0; i < M; ++i) {
+            float e = tb.at[i][j], o = tb.at[i][j + 1];
+            if (i % 2 == 0 ? (e != o) : (e != -o)) return false;
+        }
+    }
+    return true;
+}
+static_assert(pair_structure_holds<2>() && pair_structure_holds<4>() && pair_structure_holds<6>(),
+              "B^T rows / A^T columns of +-p points must pair up");
+
+// acc (op)= c * v with a compile-time coefficient; `first` starts the sum.
+__device__ __forceinline__ void mac(float &acc, bool &first, float c, float v) {
+    if (c == 0.0f) return;
+    if (first) {
+        acc = (c == 1.0f) ? v : (c == -1.0f) ? -v : c * v;
+        first = false;
+    } else {
+        acc = (c == 1.0f) ? acc + v : (c == -1.0f) ? acc - v : __builtin_fmaf(c, v, acc);
+    }
+}
+
+// out[i*SO] = sum_a B^T[i][a] in[a*SI], i, a < T.
+template <int M, int SI, int SO>
+__device__ __forceinline__ void bt_1d(const float *in, float *out) {
+    constexpr Tables<M> tb{};
+    constexpr int T = M + 2;
+    {   // p = 0 and the point at infinity: plain rows
+        float a0 = 0.f, a1 = 0.f;
+        bool f0 = true, f1 = true;
+#pragma unroll
+        for (int a = 0; a < T; ++a) {
+            mac(a0, f0, tb.bt[0][a], in[a * SI]);
+            mac(a1, f1, tb.bt[T - 1][a], in[a * SI]);
+        }
+        out[0] = a0;
+        out[(T - 1) * SO] = a1;
+    }
+#pragma unroll
+    for (int j = 1; j + 1 < T - 1; j += 2) {  // (+p, -p) rows: even part +- odd part
+        float e = 0.f, o = 0.f;
+        bool fe = true, fo = true;
+#pragma unroll
+        for (int a = 0; a < T; a += 2) mac(e, fe, tb.bt[j][a], in[a * SI]);
+#pragma unroll
+        for (int a = 1; a < T; a += 2) mac(o, fo, tb.bt[j][a], in[a * SI]);
+        out[j * SO] = e + o;
+        out[(j + 1) * SO] = e - o;
+    }
+}
+
+// out[i*SO] = sum_j A^T[i][j] in[j*SI], i < M, j < T.
+template <int M, int SI, int SO>
+__device__ __forceinline__ void at_1d(const float *in, float *out) {
+    constexpr Tables<M> tb{};
+    constexpr int T = M + 2;
+    constexpr int NP = (T - 2) / 2;  // number of (+p, -p) pairs
+    float s[NP], d[NP];
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+        s[q] = in[(1 + 2 * q) * SI] + in[(2 + 2 * q) * SI];
+        d[q] = in[(1 + 2 * q) * SI] - in[(2 + 2 * q) * SI];
+    }
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+        float acc = 0.f;
+        bool first = true;
+        mac(acc, first, tb.at[i][0], in[0]);
+#pragma unroll
+        for (int q = 0; q < NP; ++q) mac(acc, first, tb.at[i][1 + 2 * q], (i % 2 == 0) ? s[q] : d[q]);
+        mac(acc, first, tb.at[i][T - 1], in[(T - 1) * SI]);
+        out[i * SO] = acc;
+    }
+}
+
+// U = B^T d B for a T x T tile held row-major in d; U row-major, frequency i*T + j.
+template <int M>
+__device__ __forceinline__ void input_tile_transform(const float *d, float *u) {
+    constexpr int T = M + 2;
+    float tmp[T * T];
+#pragma unroll
+    for (int b = 0; b < T; ++b) bt_1d<M, T, T>(d + b, tmp + b);       // columns: B^T d
+#pragma unroll
+    for (int i = 0; i < T; ++i) bt_1d<M, 1, 1>(tmp + i * T, u + i * T);  // rows: (B^T d) B
+}
+
+// Y = A^T Mm A for a T x T tile Mm (row-major); Y is M x M row-major.
+template <int M>
+__device__ __forceinline__ void output_tile_transform(const float *mm, float *yv) {
+    constexpr int T = M + 2;
+    float tmp[M * T];
+#pragma unroll
+    for (int b = 0; b < T; ++b) at_1d<M, T, T>(mm + b, tmp + b);      // columns: A^T Mm
+#pragma unroll
+    for (int i = 0; i < M; ++i) at_1d<M, 1, 1>(tmp + i * T, yv + i * M);  // rows: (A^T Mm) A
+}
+
+// W' = G g G^T for a 3 x 3 kernel g (row-major); W' is T x T row-major.
+template <int M>
+__device__ __forceinline__ void kernel_tile_transform(const float *g, float *wt) {
+    constexpr Tables<M> tb{};
+    constexpr int T = M + 2;
+    float tmp[T * 3];
+#pragma unroll
+    for (int i = 0; i < T; ++i)
+#pragma unroll
+        for (int v = 0; v < 3; ++v) {
+            float acc = 0.f;
+            bool first = true;
+#pragma unroll
+            for (int u = 0; u < 3; ++u) mac(acc, first, tb.g[i][u], g[u * 3 + v]);
+            tmp[i * 3 + v] = first ? 0.f : acc;
+        }
+#pragma unroll
+    for (int i = 0; i < T; ++i)
+#pragma unroll
+        for (int j = 0; j < T; ++j) {
+            float acc = 0.f;
+            bool first = true;
+#pragma unroll
+            for (int v = 0; v < 3; ++v) mac(acc, first, tb.g[j][v], tmp[i * 3 + v]);
+            wt[i * T + j] = first ? 0.f : acc;
+        }
+}
+
+}  // namespace wino

@@ -1,0 +1,227 @@
+"""Python binding of ``include/wino_conv.h`` (ctypes; argument marshalling only).
+
+The functions keep the C names.  Every computation runs in the HIP library
+``libwino_conv.so``; if it is not built, the first call raises ``ImportError``
+(there is no fallback).  Tensors may be passed as torch CUDA tensors (checked for
+dtype float32, device and contiguity) or as raw device addresses (int).
+"""
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libwino_conv.so")
+
+WINO_OK, WINO_EINVAL, WINO_EUNSUPPORTED, WINO_ENOMEM, WINO_EHIP = 0, -1, -2, -3, -4
+WINO_ALGO_FUSED, WINO_ALGO_THREE_STAGE = 0, 1
+WINO_BUF_WEIGHTS, WINO_BUF_INPUT, WINO_BUF_PRODUCT = 0, 1, 2
+
+ALGOS = {"fused": WINO_ALGO_FUSED, "three_stage": WINO_ALGO_THREE_STAGE}
+
+# Every symbol the header declares, with (restype, argtypes).
+_vp = ctypes.c_void_p
+_i = ctypes.c_int
+SIGNATURES = {
+    "wino_conv_plan": (_vp, [_i, _i, _i, _i, _i, _i]),
+    "wino_conv_plan_ex": (_vp, [_i, _i, _i, _i, _i, _i, _i, _vp]),
+    "wino_conv_run": (_i, [_vp, _vp, _vp, _vp, _vp]),
+    "wino_conv_set_weights": (_i, [_vp, _vp, _vp]),
+    "wino_conv_run_pretransformed": (_i, [_vp, _vp, _vp, _vp]),
+    "wino_conv_destroy": (None, [_vp]),
+    "wino_conv_workspace_bytes": (ctypes.c_size_t, [_vp]),
+    "wino_conv_info": (_i, [_vp, ctypes.POINTER(ctypes.c_longlong),
+                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
+    "wino_conv_intermediate_dims": (_i, [_vp, _i, ctypes.POINTER(ctypes.c_longlong)]),
+    "wino_conv_copy_intermediate": (_i, [_vp, _i, ctypes.POINTER(ctypes.c_float), ctypes.c_size_t]),
+    "wino_last_error": (ctypes.c_char_p, []),
+}
+
+
+class WinoTuning(ctypes.Structure):
+    _fields_ = [("k_blocks_per_wave", ctypes.c_int), ("waves_per_group", ctypes.c_int),
+                ("reserved0", ctypes.c_int), ("reserved1", ctypes.c_int)]
+
+
+class WinoError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"wino status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises ImportError if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_1912_02165_amd.build` (hipcc, gfx950)")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(l, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = l
+    return _lib
+
+
+def wino_last_error():
+    msg = lib().wino_last_error()
+    return msg.decode() if msg else ""
+
+
+def _check(status):
+    if status != WINO_OK:
+        raise WinoError(status, wino_last_error())
+    return status
+
+
+def _ptr(t, name):
+    """Device address of a float32 contiguous CUDA tensor, or an int address."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor or an int address")
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name}: expected float32, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: expected a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def wino_conv_plan(N, C, K, H, W, m):
+    p = lib().wino_conv_plan(N, C, K, H, W, m)
+    if not p:
+        raise WinoError(WINO_EINVAL, wino_last_error())
+    return p
+
+
+def wino_conv_plan_ex(N, C, K, H, W, m, algo=WINO_ALGO_FUSED, tuning=None):
+    if isinstance(algo, str):
+        algo = ALGOS[algo]
+    t = None
+    if tuning is not None:
+        t = ctypes.byref(tuning if isinstance(tuning, WinoTuning) else WinoTuning(**tuning))
+    p = lib().wino_conv_plan_ex(N, C, K, H, W, m, algo, t)
+    if not p:
+        raise WinoError(WINO_EINVAL, wino_last_error())
+    return p
+
+
+def wino_conv_run(plan, x, w, y, stream=None):
+    return _check(lib().wino_conv_run(plan, _ptr(x, "x"), _ptr(w, "w"), _ptr(y, "y"),
+                                      _stream(stream)))
+
+
+def wino_conv_set_weights(plan, w, stream=None):
+    return _check(lib().wino_conv_set_weights(plan, _ptr(w, "w"), _stream(stream)))
+
+
+def wino_conv_run_pretransformed(plan, x, y, stream=None):
+    return _check(lib().wino_conv_run_pretransformed(plan, _ptr(x, "x"), _ptr(y, "y"),
+                                                     _stream(stream)))
+
+
+def wino_conv_destroy(plan):
+    lib().wino_conv_destroy(plan)
+
+
+def wino_conv_workspace_bytes(plan):
+    return int(lib().wino_conv_workspace_bytes(plan))
+
+
+def wino_conv_info(plan):
+    """(n_tiles, direct_flops, tdomain_flops)."""
+    nt, df, tf = ctypes.c_longlong(), ctypes.c_double(), ctypes.c_double()
+    _check(lib().wino_conv_info(plan, ctypes.byref(nt), ctypes.byref(df), ctypes.byref(tf)))
+    return nt.value, df.value, tf.value
+
+
+def wino_conv_intermediate_dims(plan, which):
+    dims = (ctypes.c_longlong * 4)()
+    _check(lib().wino_conv_intermediate_dims(plan, which, dims))
+    return tuple(int(d) for d in dims)
+
+
+def wino_conv_copy_intermediate(plan, which):
+    """Copy an intermediate buffer to a new float32 NumPy array shaped by its dims."""
+    import numpy as np
+    dims = wino_conv_intermediate_dims(plan, which)
+    out = np.empty(dims, dtype=np.float32)
+    _check(lib().wino_conv_copy_intermediate(
+        plan, which, out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), out.size))
+    return out
+
+
+class Plan:
+    """Owning wrapper of a plan handle (``with Plan(...) as p: p.run(x, w, y)``)."""
+
+    def __init__(self, N, C, K, H, W, m, algo="fused", tuning=None):
+        self.shape = (N, C, K, H, W)
+        self.m = m
+        self.algo = algo
+        self.handle = wino_conv_plan_ex(N, C, K, H, W, m, algo, tuning)
+
+    def run(self, x, w, y, stream=None):
+        wino_conv_run(self.handle, x, w, y, stream)
+
+    def set_weights(self, w, stream=None):
+        wino_conv_set_weights(self.handle, w, stream)
+
+    def run_pretransformed(self, x, y, stream=None):
+        wino_conv_run_pretransformed(self.handle, x, y, stream)
+
+    def info(self):
+        return wino_conv_info(self.handle)
+
+    def workspace_bytes(self):
+        return wino_conv_workspace_bytes(self.handle)
+
+    def intermediate(self, which):
+        return wino_conv_copy_intermediate(self.handle, which)
+
+    def close(self):
+        if self.handle:
+            wino_conv_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def conv2d(x, w, m=4, algo="fused", stream=None):
+    """y = 3x3 conv of x (N,C,H,W) with w (K,C,3,3), stride 1, pad 1, via the library."""
+    import torch
+    N, C, H, W = x.shape
+    K = w.shape[0]
+    y = torch.empty((N, K, H, W), dtype=torch.float32, device=x.device)
+    with Plan(N, C, K, H, W, m, algo) as p:
+        p.run(x, w, y, stream)
+        # the plan's workspace must outlive the queued work
+        (torch.cuda.current_stream() if stream is None else stream).synchronize()
+    return y

@@ -1,0 +1,207 @@
+"""GPU parity: the HIP library (through the C ABI) against the CPU oracle.
+
+* small and ragged shapes (several tiles and workgroups, C and K not multiples of
+  4 or 16, images smaller than a tile) against the full fp64 direct convolution;
+* the 56x56 layer (N=1, C=K=64) in full at every m it runs with;
+* the full-size VGG/ResNet-shaped layers in the launch configuration the
+  benchmark times, on sampled output planes the oracle computes one by one;
+* both algorithms (fused and three-stage) everywhere.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_1912_02165_amd as wc
+from paper_1912_02165_amd import workloads
+from oracle.direct import direct_conv, direct_conv_planes
+from parity import assert_close
+
+pytestmark = pytest.mark.gpu
+
+ALGOS = ("fused", "three_stage")
+
+SMALL = [
+    (1, 1, 1, 1, 1), (1, 2, 3, 2, 5), (1, 3, 4, 1, 9), (1, 3, 5, 7, 9), (2, 4, 16, 8, 8),
+    (1, 5, 17, 13, 11), (3, 8, 20, 17, 23), (2, 37, 45, 29, 35), (2, 16, 33, 30, 31),
+    (1, 64, 64, 20, 20), (4, 12, 40, 6, 6), (1, 130, 18, 9, 10),
+]
+
+
+def run_gpu(x, w, m, algo, tuning=None):
+    N, C, H, W = x.shape
+    K = w.shape[0]
+    xd = torch.from_numpy(x).cuda()
+    wd = torch.from_numpy(w).cuda()
+    y = torch.full((N, K, H, W), float("nan"), dtype=torch.float32, device="cuda")
+    with wc.Plan(N, C, K, H, W, m, algo, tuning) as p:
+        p.run(xd, wd, y)
+        torch.cuda.synchronize()
+    return y
+
+
+def rand(shape, seed):
+    return np.random.default_rng(seed).uniform(-1, 1, size=shape).astype(np.float32)
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+@pytest.mark.parametrize("m", (2, 4, 6))
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: "x".join(map(str, s)))
+def test_small_shapes(algo, m, shape):
+    N, C, K, H, W = shape
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=sum(shape) + m)
+    print(f"\n[gpu] small {algo} m={m} shape={shape}", flush=True)
+    y = run_gpu(x, w, m, algo).cpu().numpy()
+    assert_close(y, direct_conv(x, w), m, f"{algo} F({m}) {shape}")
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+@pytest.mark.parametrize("m", (2, 4))
+def test_layer1_full(algo, m):
+    layer = workloads.LAYER_BY_ID[1]
+    x, w = workloads.layer_inputs(layer)
+    print(f"\n[gpu] {layer.tag(m)} {algo}", flush=True)
+    y = run_gpu(x, w, m, algo).cpu().numpy()
+    rel, mx = assert_close(y, direct_conv(x, w), m, f"{layer.tag(m)} {algo}")
+    print(f"rel_l2={rel:.3e} max={mx:.3e}")
+
+
+def sample_planes(N, K, seed, count=8):
+    rng = np.random.default_rng(seed)
+    planes = {(0, 0), (N - 1, K - 1), (N // 2, K // 3), (min(1, N - 1), K - 1), (N - 1, 0)}
+    while len(planes) < count:
+        planes.add((int(rng.integers(N)), int(rng.integers(K))))
+    return sorted(planes)
+
+
+FULL_PAIRS = [(l, m) for (l, m) in workloads.PAIRS if l.id != 1]
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+@pytest.mark.parametrize("pair", FULL_PAIRS, ids=lambda p: p[0].tag(p[1]))
+def test_full_layers_sampled(algo, pair):
+    layer, m = pair
+    x, w = workloads.layer_inputs(layer)
+    print(f"\n[gpu] {layer.tag(m)} {algo} full size", flush=True)
+    y = run_gpu(x, w, m, algo)
+    assert bool(torch.isfinite(y).all()), "non-finite output"
+    planes = sample_planes(layer.N, layer.K, seed=layer.id * 10 + m)
+    n_idx = torch.tensor([p[0] for p in planes], device="cuda")
+    k_idx = torch.tensor([p[1] for p in planes], device="cuda")
+    got = y[n_idx, k_idx].cpu().numpy()
+    ref = direct_conv_planes(x, w, planes)
+    rel, mx = assert_close(got, ref, m, f"{layer.tag(m)} {algo} planes {planes}")
+    print(f"rel_l2={rel:.3e} max={mx:.3e} over {len(planes)} planes")
+
+
+@pytest.mark.parametrize("m", (2, 4, 6))
+def test_three_stage_intermediates(m):
+    """Each unfused stage against the fp64 CPU Winograd's matching intermediate."""
+    from oracle import winograd
+    N, C, K, H, W = 2, 6, 20, 11, 13
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=70 + m)
+    T2 = (m + 2) ** 2
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    y = torch.empty((N, K, H, W), device="cuda")
+    with wc.Plan(N, C, K, H, W, m, "three_stage") as p:
+        p.run(xd, wd, y)
+        torch.cuda.synchronize()
+        wt = p.intermediate(wc.WINO_BUF_WEIGHTS)       # (Kb, Cs, T2, 64) operand order
+        U = p.intermediate(wc.WINO_BUF_INPUT)          # (T2, Cp, tiles_p, 1)
+        Mf = p.intermediate(wc.WINO_BUF_PRODUCT)       # (T2, Kp, tiles_p, 1)
+    Wt_ref = winograd.weight_transform(w, m)             # (T2, C, K)
+    U_ref = winograd.input_transform(x, m)               # (T2, C, ntiles)
+    M_ref = winograd.frequency_gemm(U_ref, Wt_ref)       # (T2, K, ntiles)
+    ntiles = U_ref.shape[2]
+    # undo the operand order: [kb][cs][f/4][lane][f%4], lane = (c%4)*16 + k%16
+    Kb, Cs = wt.shape[:2]
+    flat = wt.reshape(Kb, Cs, T2 // 4, 64, 4)
+    wt_fck = np.empty((T2, Cs * 4, Kb * 16), np.float32)
+    for f in range(T2):
+        blk = flat[:, :, f // 4, :, f % 4].reshape(Kb, Cs, 4, 16)   # kb, cs, c%4, k%16
+        wt_fck[f] = blk.transpose(1, 2, 0, 3).reshape(Cs * 4, Kb * 16)
+    np.testing.assert_allclose(wt_fck[:, :C, :K], Wt_ref, rtol=1e-6, atol=1e-7)
+    assert not wt_fck[:, C:, :].any() and not wt_fck[:, :, K:].any()
+    U = U[..., 0]
+    scale = np.abs(U_ref).max()
+    np.testing.assert_allclose(U[:, :C, :ntiles], U_ref, rtol=0, atol=1e-6 * scale)
+    assert not U[:, C:, :].any() and not U[:, :, ntiles:].any()
+    Mf = Mf[..., 0]
+    scale = np.abs(M_ref).max()
+    np.testing.assert_allclose(Mf[:, :K, :ntiles], M_ref, rtol=0, atol=1e-5 * scale)
+    assert_close(y.cpu().numpy(), direct_conv(x, w), m, "three-stage end to end")
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+def test_deterministic(algo):
+    x, w = workloads.random_inputs(3, 40, 48, 30, 26, seed=5)
+    a = run_gpu(x, w, 4, algo)
+    b = run_gpu(x, w, 4, algo)
+    assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+def test_guard_regions_untouched(algo):
+    N, C, K, H, W = 2, 8, 24, 9, 14
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=6)
+    n = N * K * H * W
+    buf = torch.full((n + 2 * 1024,), float("nan"), device="cuda")
+    y = buf[1024:1024 + n].view(N, K, H, W)
+    with wc.Plan(N, C, K, H, W, 4, algo) as p:
+        p.run(torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda(), y)
+        torch.cuda.synchronize()
+    assert torch.isnan(buf[:1024]).all() and torch.isnan(buf[1024 + n:]).all()
+    assert_close(y.cpu().numpy(), direct_conv(x, w), 4, "guarded")
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+def test_pretransformed_matches_run(algo):
+    N, C, K, H, W = 2, 20, 36, 15, 16
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=7)
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    y1 = torch.empty((N, K, H, W), device="cuda")
+    y2 = torch.empty_like(y1)
+    with wc.Plan(N, C, K, H, W, 6, algo) as p:
+        with pytest.raises(wc.WinoError):
+            p.run_pretransformed(xd, y2)       # no kernels set yet
+        p.run(xd, wd, y1)
+        p.set_weights(wd)
+        p.run_pretransformed(xd, y2)
+        torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+
+
+def test_tuning_overrides_agree():
+    x, w = workloads.random_inputs(2, 24, 64, 21, 19, seed=8)
+    ref = direct_conv(x, w)
+    for m, nkbs in ((2, (1, 2, 4)), (4, (1, 2)), (6, (1,))):
+        for nkb in nkbs:
+            for waves in (1, 2, 4):
+                y = run_gpu(x, w, m, "fused", {"k_blocks_per_wave": nkb, "waves_per_group": waves})
+                assert_close(y.cpu().numpy(), ref, m, f"F({m}) nkb={nkb} waves={waves}")
+
+
+def test_bad_pointers_rejected():
+    N, C, K, H, W = 1, 4, 4, 8, 8
+    xd = torch.zeros((N, C, H, W), device="cuda")
+    wd = torch.zeros((K, C, 3, 3), device="cuda")
+    with wc.Plan(N, C, K, H, W, 4) as p:
+        with pytest.raises(wc.WinoError, match="overlaps"):
+            p.run(xd, wd, xd)
+        host = np.zeros(N * K * H * W, np.float32)
+        with pytest.raises(wc.WinoError, match="device"):
+            p.run(xd, wd, host.ctypes.data)
+        with pytest.raises(wc.WinoError, match="aligned"):
+            p.run(xd, wd, xd.data_ptr() + 2)
+    # an allocation too small for the tensor
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    ptr = ctypes.c_void_p()
+    assert hip.hipMalloc(ctypes.byref(ptr), ctypes.c_size_t(1024)) == 0
+    try:
+        with wc.Plan(1, 4, 4, 64, 64, 4) as p:
+            with pytest.raises(wc.WinoError, match="allocation holds"):
+                p.run(torch.zeros((1, 4, 64, 64), device="cuda"), torch.zeros((4, 4, 3, 3), device="cuda"),
+                      ptr.value)
+    finally:
+        hip.hipFree(ptr)
