@@ -64,14 +64,26 @@ enum {
     WINO_BUF_PRODUCT = 2    /* three-stage only: per-frequency products    */
 };
 
-/* Optional blocking overrides; a field of 0 keeps the automatic choice.
- *   k_blocks_per_wave: output channels per wave, in blocks of 16 (fused).
- *   waves_per_group:   waves (of 64 lanes, 16 tiles each) per workgroup (fused). */
+/* Fused-kernel schedules (wino_tuning.schedule). */
+enum {
+    WINO_SCHED_AUTO = 0,
+    WINO_SCHED_SHARED = 1,   /* a workgroup transforms each input tile once into LDS and
+                                shares it across 64 output channels (default) */
+    WINO_SCHED_PER_WAVE = 2  /* every wave transforms its own input tiles in registers */
+};
+
+/* Optional blocking overrides for the fused algorithm; a field of 0 keeps the
+ * automatic choice.
+ *   schedule:          WINO_SCHED_*.
+ *   k_blocks_per_wave: per-wave schedule: output channels per wave, in blocks of 16.
+ *   waves_per_group:   per-wave schedule: waves (16 tiles each) per workgroup, 1..4.
+ *   tile_blocks:       shared schedule: tiles per workgroup in blocks of 16 (1, or 2
+ *                      for m <= 4). */
 typedef struct {
+    int schedule;
     int k_blocks_per_wave;
     int waves_per_group;
-    int reserved0;
-    int reserved1;
+    int tile_blocks;
 } wino_tuning;
 
 /* Create a plan for an F(m x m, 3 x 3) convolution of an N x C x H x W input

@@ -198,16 +198,20 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
     }
     FusedCfg cfg = wino::fused_cfg_default(g);
     if (t) {
-        if (t->k_blocks_per_wave < 0 || t->waves_per_group < 0) {
+        if (t->schedule < 0 || t->k_blocks_per_wave < 0 || t->waves_per_group < 0 ||
+            t->tile_blocks < 0) {
             set_err("tuning fields must be >= 0");
             return nullptr;
         }
+        if (t->schedule) cfg.schedule = t->schedule;
         if (t->k_blocks_per_wave) cfg.nkb = t->k_blocks_per_wave;
         if (t->waves_per_group) cfg.waves = t->waves_per_group;
+        if (t->tile_blocks) cfg.tb = t->tile_blocks;
     }
     if (algo == WINO_ALGO_FUSED && !wino::fused_cfg_supported(m, cfg)) {
-        set_err("fused blocking k_blocks_per_wave=%d waves_per_group=%d is not built for m=%d",
-                cfg.nkb, cfg.waves, m);
+        set_err("fused schedule %d (k_blocks_per_wave=%d waves_per_group=%d tile_blocks=%d) "
+                "is not built for m=%d",
+                cfg.schedule, cfg.nkb, cfg.waves, cfg.tb, m);
         return nullptr;
     }
     const size_t wt_bytes = (size_t)g.Kb_alloc * 16 * g.Cs * 4 * g.T2 * sizeof(float);
@@ -251,10 +255,10 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
     }
     if (log_enabled())
         fprintf(stderr,
-                "[wino] plan N=%d C=%d K=%d H=%d W=%d m=%d algo=%s tiles=%d nkb=%d waves=%d "
-                "workspace=%zu B\n",
+                "[wino] plan N=%d C=%d K=%d H=%d W=%d m=%d algo=%s tiles=%d schedule=%d tb=%d "
+                "nkb=%d waves=%d workspace=%zu B\n",
                 N, C, K, H, W, m, algo == WINO_ALGO_FUSED ? "fused" : "three_stage", g.ntiles,
-                cfg.nkb, cfg.waves, wt_bytes + U_bytes + M_bytes);
+                cfg.schedule, cfg.tb, cfg.nkb, cfg.waves, wt_bytes + U_bytes + M_bytes);
     return p;
 oom:
     (void)hipGetLastError();

@@ -20,10 +20,13 @@ struct Geometry {
     int tiles_p;        // ntiles rounded up to a multiple of 64 (three-stage buffers)
 };
 
-// Fused-kernel blocking.
+// Fused-kernel schedule and blocking.
+enum { kSchedShared = 1, kSchedPerWave = 2, kSchedSpecialised = 3 };
 struct FusedCfg {
-    int nkb;    // 16-channel output blocks per wave
-    int waves;  // waves per workgroup (each owns 16 tiles)
+    int schedule;  // kSchedShared, kSchedPerWave or kSchedSpecialised
+    int tb;        // shared: tile blocks of 16 per workgroup
+    int nkb;       // per-wave: 16-channel output blocks per wave
+    int waves;     // per-wave: waves per workgroup (each owns 16 tiles)
 };
 
 // Kernel transform: w (K x C x 3 x 3) -> wt in matrix-core operand order.

@@ -116,20 +116,113 @@ __global__ void __launch_bounds__(256) weight_transform_kernel(const float *__re
 }
 
 // ---------------------------------------------------------------------------
+// Buffer-resource loads of input tiles.  A raw buffer load whose byte offset is
+// at or past the resource's size returns 0 without touching memory, which gives
+// the implicit zero padding of Sec. 2.1 with unconditional loads: offsets of rows
+// or columns outside the image are pushed to >= 2^31 (x is below 2^31 bytes) with
+// a saturating add.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float *base, unsigned bytes) {
+    // dword3 = 0x00020000: 32-bit data format, as raw buffer loads on gfx9 expect
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+constexpr unsigned kOutside = 0x80000000u;
+
+// Per-lane byte offsets of the T x T input tile (rows ty*M-1+a, columns tx*M-1+b)
+// of one tile and channel lane_c, relative to the plane of channel 0 of the
+// current channel step.  PRECOMP keeps all T^2 offsets in registers; otherwise
+// each element costs one saturating add.
+template <int M, bool PRECOMP>
+struct BufTile {
+    static constexpr int T = M + 2, T2 = T * T;
+    unsigned off[PRECOMP ? T2 : 1];
+    unsigned roff[PRECOMP ? 1 : T];
+    unsigned coff[PRECOMP ? 1 : T];
+
+    __device__ __forceinline__ void init(const Geometry &g, const TileIdx &t, int lane_c) {
+        const unsigned base = (unsigned)(((long long)t.n * g.C + lane_c) * g.H * g.W) * 4u;
+        unsigned ro[T], co[T];
+#pragma unroll
+        for (int a = 0; a < T; ++a) {
+            const int h = t.ty * M - 1 + a;
+            ro[a] = (t.ok && h >= 0 && h < g.H) ? base + (unsigned)(h * g.W) * 4u : kOutside;
+        }
+#pragma unroll
+        for (int b = 0; b < T; ++b) {
+            const int w = t.tx * M - 1 + b;
+            co[b] = (w >= 0 && w < g.W) ? (unsigned)w * 4u : kOutside;
+        }
+        if constexpr (PRECOMP) {
+#pragma unroll
+            for (int a = 0; a < T; ++a)
+#pragma unroll
+                for (int b = 0; b < T; ++b) off[a * T + b] = __builtin_elementwise_add_sat(ro[a], co[b]);
+        } else {
+#pragma unroll
+            for (int a = 0; a < T; ++a) roff[a] = ro[a];
+#pragma unroll
+            for (int b = 0; b < T; ++b) coff[b] = co[b];
+        }
+    }
+
+    __device__ __forceinline__ unsigned offset(int a, int b) const {
+        if constexpr (PRECOMP) return off[a * T + b];
+        else return __builtin_elementwise_add_sat(roff[a], coff[b]);
+    }
+
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, float *d) const {
+#pragma unroll
+        for (int a = 0; a < T; ++a)
+#pragma unroll
+            for (int b = 0; b < T; ++b)
+                d[a * T + b] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, offset(a, b), 0, 0));
+    }
+};
+
+// ---------------------------------------------------------------------------
 // Fused kernel (Sec. 4: a task of R tiles does input transform -> T^2 products
 // against the hot kernel matrices -> output transform).  Here a task is a
 // workgroup of `waves` waves; each wave owns 16 consecutive tiles and the same
 // NKB blocks of 16 output channels.  Per 4-channel step a lane loads one input
 // tile, transforms it in registers (B^T d B) and feeds each frequency to the
 // matrix core against the matching transformed-kernel slice, which every wave
-// of the workgroup reads from the same cached lines.  The accumulators (the
-// paper's result matrices) never leave registers; after the last step each lane
-// inverse-transforms its tile for its four output channels and writes y.
+// of the workgroup reads from the same cached lines.  The next step's input tile
+// is loaded while the current one is transformed and multiplied.  The
+// accumulators (the paper's result matrices) never leave registers; after the
+// last step each lane inverse-transforms its tile for its four output channels
+// and writes y.
+template <int M, int NKB>
+__device__ __forceinline__ void fused_step(floatx4 (&acc)[NKB][(M + 2) * (M + 2)], const float *d,
+                                           const floatx4 *__restrict__ wt, const Geometry &g,
+                                           int kb0, int cs, int lane, bool zero_u) {
+    constexpr int T = M + 2, T2 = T * T;
+    float u[T2];
+    input_tile_transform<M>(d, u);
+    if (zero_u) {  // channel past C in the last step (only when C % 4 != 0)
+#pragma unroll
+        for (int f = 0; f < T2; ++f) u[f] = 0.0f;
+    }
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+        const floatx4 *wp = wt + ((long long)(kb0 + kb) * g.Cs + cs) * (T2 / 4) * 64 + lane;
+#pragma unroll
+        for (int f4 = 0; f4 < T2 / 4; ++f4) {
+            const floatx4 a = wp[f4 * 64];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                acc[kb][4 * f4 + q] =
+                    __builtin_amdgcn_mfma_f32_16x16x4f32(a[q], u[4 * f4 + q], acc[kb][4 * f4 + q], 0, 0, 0);
+        }
+    }
+}
+
 template <int M, int NKB>
 __global__ void __launch_bounds__(256) fused_kernel(const float *__restrict__ x,
                                                     const floatx4 *__restrict__ wt,
                                                     float *__restrict__ y, Geometry g) {
     constexpr int T = M + 2, T2 = T * T;
+    constexpr bool PRECOMP = (M <= 2);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int waves = blockDim.x >> 6;
@@ -137,10 +230,12 @@ __global__ void __launch_bounds__(256) fused_kernel(const float *__restrict__ x,
     const int cq = lane >> 4;
     const int kb0 = blockIdx.y * NKB;
     const TileIdx ti = decode_tile(g, tile);
-    TileLoader<M> ld;
-    ld.init(g, ti);
+    BufTile<M, PRECOMP> ld;
+    ld.init(g, ti, cq);
     const long long HW = (long long)g.H * g.W;
-    const float *xn = x + (long long)ti.n * g.C * HW;
+    const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
+    const unsigned step_bytes = (unsigned)(4 * HW * 4);
+    const bool ctail = (g.C & 3) != 0;
 
     floatx4 acc[NKB][T2];
 #pragma unroll
@@ -148,26 +243,18 @@ __global__ void __launch_bounds__(256) fused_kernel(const float *__restrict__ x,
 #pragma unroll
         for (int f = 0; f < T2; ++f) acc[kb][f] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    for (int cs = 0; cs < g.Cs; ++cs) {
-        const int c = cs * 4 + cq;
-        const bool cok = c < g.C;
-        float d[T2];
-        ld.load(xn + (cok ? c : 0) * HW, cok, d);
-        float u[T2];
-        input_tile_transform<M>(d, u);
-#pragma unroll
-        for (int kb = 0; kb < NKB; ++kb) {
-            const floatx4 *wp = wt + ((long long)(kb0 + kb) * g.Cs + cs) * (T2 / 4) * 64 + lane;
-#pragma unroll
-            for (int f4 = 0; f4 < T2 / 4; ++f4) {
-                const floatx4 a = wp[f4 * 64];
-                acc[kb][4 * f4 + 0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], u[4 * f4 + 0], acc[kb][4 * f4 + 0], 0, 0, 0);
-                acc[kb][4 * f4 + 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], u[4 * f4 + 1], acc[kb][4 * f4 + 1], 0, 0, 0);
-                acc[kb][4 * f4 + 2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], u[4 * f4 + 2], acc[kb][4 * f4 + 2], 0, 0, 0);
-                acc[kb][4 * f4 + 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], u[4 * f4 + 3], acc[kb][4 * f4 + 3], 0, 0, 0);
-            }
-        }
+    float dA[T2], dB[T2];
+    ld.load(make_rsrc(x, xbytes), dA);
+    int cs = 0;
+    for (; cs + 1 < g.Cs; cs += 2) {
+        ld.load(make_rsrc(x + (cs + 1) * 4 * HW, xbytes - (cs + 1) * step_bytes), dB);
+        fused_step<M, NKB>(acc, dA, wt, g, kb0, cs, lane, false);
+        if (cs + 2 < g.Cs) ld.load(make_rsrc(x + (cs + 2) * 4 * HW, xbytes - (cs + 2) * step_bytes), dA);
+        fused_step<M, NKB>(acc, dB, wt, g, kb0, cs + 1, lane,
+                           ctail && cs + 1 == g.Cs - 1 && (cs + 1) * 4 + cq >= g.C);
     }
+    if (cs < g.Cs)
+        fused_step<M, NKB>(acc, dA, wt, g, kb0, cs, lane, ctail && cs * 4 + cq >= g.C);
 
     // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
 #pragma unroll
@@ -194,6 +281,300 @@ __global__ void __launch_bounds__(256) fused_kernel(const float *__restrict__ x,
                     }
                 }
             }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Fused kernel, shared-transform schedule.  A workgroup (4 waves) is one task of
+// R = 16*TB tiles and 64 output channels (Sec. 4).  The channel loop runs in
+// stages of CC = 256/R channels; in each stage every thread loads and transforms
+// one (tile, channel) input tile and stores its T^2 values in LDS, so the
+// left-hand matrices of the stage (the paper's R x C slices, one per frequency)
+// are built once and read by all four waves.  Wave w multiplies them by the
+// transformed kernels of output-channel block w, which stream from L2 (the
+// paper's hot right-hand matrices).  LDS is double-buffered: while a stage's
+// products run, the next stage's input tiles are loaded and then transformed
+// into the other buffer, with one barrier per stage.  The accumulators (result
+// matrices) stay in registers until the output transform.
+//
+// LDS layout of one buffer, in float4 units: [T^2/4][CC][R] with the four
+// frequencies 4*f4 .. 4*f4+3 of (channel, tile) in one float4, so that a wave's
+// matrix-core B operand for four frequencies is one contiguous 1 KB read.
+template <int M, int TB>
+__global__ void __launch_bounds__(256) fused_shared_kernel(const float *__restrict__ x,
+                                                           const floatx4 *__restrict__ wt,
+                                                           float *__restrict__ y, Geometry g) {
+    constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
+    constexpr int R = 16 * TB;       // tiles per workgroup
+    constexpr int CC = 256 / R;      // channels per stage
+    constexpr int SS = CC / 4;       // matrix-core channel steps per stage
+    constexpr int BUF = F4 * CC * R; // float4s per LDS buffer
+    __shared__ floatx4 lds[2 * BUF];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const long long HW = (long long)g.H * g.W;
+    const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
+    const int tile0 = blockIdx.x * R;
+
+    // transform role: thread -> (tile tile0 + tr, channel cl of the stage)
+    const int tr = tid % R;
+    const int cl = tid / R;
+    BufTile<M, (M <= 2)> ld;
+    ld.init(g, decode_tile(g, tile0 + tr), cl);
+    const int stages = (g.C + CC - 1) / CC;
+    const bool ctail = (g.C % CC) != 0;
+
+    // matrix-core role: wave -> output-channel block kb
+    const int kb = blockIdx.y * 4 + wave;
+    const floatx4 *wk = wt + (long long)kb * g.Cs * F4 * 64 + lane;
+
+    floatx4 acc[TB][T2];
+#pragma unroll
+    for (int t = 0; t < TB; ++t)
+#pragma unroll
+        for (int f = 0; f < T2; ++f) acc[t][f] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    float d[T2];
+    auto transform_store = [&](int stage, floatx4 *buf) {
+        float u[T2];
+        input_tile_transform<M>(d, u);
+        if (ctail && stage == stages - 1 && stage * CC + cl >= g.C) {
+#pragma unroll
+            for (int f = 0; f < T2; ++f) u[f] = 0.0f;
+        }
+#pragma unroll
+        for (int f4 = 0; f4 < F4; ++f4)
+            buf[(f4 * CC + cl) * R + tr] = floatx4{u[4 * f4], u[4 * f4 + 1], u[4 * f4 + 2], u[4 * f4 + 3]};
+    };
+
+    ld.load(make_rsrc(x, xbytes), d);
+    transform_store(0, lds);
+    __syncthreads();
+
+    for (int j = 0; j < stages; ++j) {
+        const bool next = j + 1 < stages;
+        if (next) {
+            const long long cbase = (long long)(j + 1) * CC * HW;
+            ld.load(make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4)), d);
+        }
+        const floatx4 *cur = lds + (j & 1) * BUF;
+#pragma unroll
+        for (int s = 0; s < SS; ++s) {
+            const int cs = j * SS + s;
+            if (cs < g.Cs) {
+                const floatx4 *wp = wk + (long long)cs * F4 * 64;
+                const floatx4 *bp = cur + (4 * s + (lane >> 4)) * R + (lane & 15);
+#pragma unroll
+                for (int f4 = 0; f4 < F4; ++f4) {
+                    const floatx4 a = wp[f4 * 64];
+#pragma unroll
+                    for (int t = 0; t < TB; ++t) {
+                        const floatx4 b = bp[f4 * CC * R + t * 16];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            acc[t][4 * f4 + q] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                a[q], b[q], acc[t][4 * f4 + q], 0, 0, 0);
+                    }
+                }
+            }
+        }
+        if (next) transform_store(j + 1, lds + ((j + 1) & 1) * BUF);
+        __syncthreads();
+    }
+
+    // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
+#pragma unroll
+    for (int t = 0; t < TB; ++t) {
+        const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int k = kb * 16 + (lane >> 4) * 4 + v;
+            float mm[T2];
+#pragma unroll
+            for (int f = 0; f < T2; ++f) mm[f] = acc[t][f][v];
+            float yy[M * M];
+            output_tile_transform<M>(mm, yy);
+            if (ti.ok && k < g.K) {
+                float *yp = y + ((long long)ti.n * g.K + k) * HW;
+#pragma unroll
+                for (int i = 0; i < M; ++i) {
+                    const int h = ti.ty * M + i;
+                    if (h < g.H) {
+#pragma unroll
+                        for (int jj = 0; jj < M; ++jj) {
+                            const int w = ti.tx * M + jj;
+                            if (w < g.W) __builtin_nontemporal_store(yy[i * M + jj], yp + (long long)h * g.W + w);
+                        }
+                    }
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Workgroups are dispatched to the 8 XCDs round-robin by linear id.  This remaps
+// the linear id so that each XCD receives one contiguous range of logical ids:
+// neighbouring tile groups then run on the same XCD and share the halo rows of
+// their input tiles (and the transformed kernels) in that XCD's L2.
+__device__ __forceinline__ int xcd_contiguous_id(int lin, int total) {
+    constexpr int kXcds = 8;
+    const int q = total / kXcds, r = total % kXcds;
+    const int xcd = lin % kXcds, idx = lin / kXcds;
+    return xcd * q + (xcd < r ? xcd : r) + idx;
+}
+
+// Store one m x m output tile of plane yp (clipped to H x W).  vec: rows may be
+// written with m-float vector stores (16-byte aligned for m = 4, 8-byte for m = 2, 6).
+template <int M>
+__device__ __forceinline__ void store_tile(float *__restrict__ yp, const float *yy, int h0, int w0,
+                                           const Geometry &g, bool vec) {
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+        const int h = h0 + i;
+        if (h >= g.H) break;
+        float *row = yp + (long long)h * g.W + w0;
+        if (vec && w0 + M <= g.W) {
+            if constexpr (M == 4) {
+                *reinterpret_cast<floatx4 *>(row) =
+                    floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]};
+            } else {
+                typedef float floatx2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+                for (int jj = 0; jj < M; jj += 2)
+                    *reinterpret_cast<floatx2 *>(row + jj) = floatx2{yy[i * M + jj], yy[i * M + jj + 1]};
+            }
+        } else {
+#pragma unroll
+            for (int jj = 0; jj < M; ++jj)
+                if (w0 + jj < g.W) row[jj] = yy[i * M + jj];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Fused kernel, warp-specialised schedule.  A workgroup of 8 waves is one task of
+// R = 16*TB tiles and 64 output channels.  Waves 4..7 are producers: per stage of
+// CC = 256/R channels each of their lanes loads one (tile, channel) input tile,
+// transforms it (B^T d B) and writes its T^2 values to LDS.  Waves 0..3 are
+// consumers: wave w multiplies the stage's transformed tiles by the transformed
+// kernels of output-channel block w on the matrix cores, with the kernel operands
+// of the next 4-channel step loaded while the current step runs.  Two waves per
+// SIMD (one of each kind) let the producers' vector work run while the matrix
+// cores are busy.  LDS is double-buffered with one barrier per stage; the layout
+// of a buffer is that of fused_shared_kernel.
+template <int M, int TB>
+__global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__ x,
+                                                       const floatx4 *__restrict__ wt,
+                                                       float *__restrict__ y, Geometry g, int vec) {
+    constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
+    constexpr int R = 16 * TB;
+    constexpr int CC = 256 / R;
+    constexpr int SS = CC / 4;
+    constexpr int BUF = F4 * CC * R;
+    __shared__ floatx4 lds[2 * BUF];
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int lin = xcd_contiguous_id(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
+    const int tgrp = lin % gridDim.x;
+    const int kgrp = lin / gridDim.x;
+    const int tile0 = tgrp * R;
+    const long long HW = (long long)g.H * g.W;
+    const int stages = (g.C + CC - 1) / CC;
+
+    if (wave >= 4) {
+        // ---------------- producer: load + input transform -> LDS ----------------
+        const int pt = tid - 256;
+        const int tr = pt % R;
+        const int cl = pt / R;
+        BufTile<M, (M <= 2)> ld;
+        ld.init(g, decode_tile(g, tile0 + tr), cl);
+        const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
+        const bool ctail = (g.C % CC) != 0;
+        for (int j = -1; j < stages; ++j) {
+            const int st = j + 1;  // stage produced in this round
+            if (st < stages) {
+                float d[T2];
+                const long long cbase = (long long)st * CC * HW;
+                ld.load(make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4)), d);
+                float u[T2];
+                input_tile_transform<M>(d, u);
+                if (ctail && st == stages - 1 && st * CC + cl >= g.C) {
+#pragma unroll
+                    for (int f = 0; f < T2; ++f) u[f] = 0.0f;
+                }
+                floatx4 *buf = lds + (st & 1) * BUF;
+#pragma unroll
+                for (int f4 = 0; f4 < F4; ++f4)
+                    buf[(f4 * CC + cl) * R + tr] =
+                        floatx4{u[4 * f4], u[4 * f4 + 1], u[4 * f4 + 2], u[4 * f4 + 3]};
+            }
+            __syncthreads();
+        }
+        return;
+    }
+
+    // ---------------- consumer: per-frequency products on the matrix cores ----------------
+    const int kb = kgrp * 4 + wave;
+    const floatx4 *wk = wt + (long long)kb * g.Cs * F4 * 64 + lane;
+    floatx4 acc[TB][T2];
+#pragma unroll
+    for (int t = 0; t < TB; ++t)
+#pragma unroll
+        for (int f = 0; f < T2; ++f) acc[t][f] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    floatx4 aw[F4];
+#pragma unroll
+    for (int f4 = 0; f4 < F4; ++f4) aw[f4] = wk[f4 * 64];
+    __syncthreads();  // stage 0 is in LDS
+    for (int j = 0; j < stages; ++j) {
+        const floatx4 *cur = lds + (j & 1) * BUF;
+#pragma unroll
+        for (int s = 0; s < SS; ++s) {
+            const int cs = j * SS + s;
+            if (cs < g.Cs) {
+                floatx4 an[F4];
+                const int cn = cs + 1 < g.Cs ? cs + 1 : cs;
+#pragma unroll
+                for (int f4 = 0; f4 < F4; ++f4) an[f4] = wk[((long long)cn * F4 + f4) * 64];
+                const floatx4 *bp = cur + (4 * s + (lane >> 4)) * R + (lane & 15);
+#pragma unroll
+                for (int f4 = 0; f4 < F4; ++f4) {
+#pragma unroll
+                    for (int t = 0; t < TB; ++t) {
+                        const floatx4 b = bp[f4 * CC * R + t * 16];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            acc[t][4 * f4 + q] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                aw[f4][q], b[q], acc[t][4 * f4 + q], 0, 0, 0);
+                    }
+                }
+#pragma unroll
+                for (int f4 = 0; f4 < F4; ++f4) aw[f4] = an[f4];
+            }
+        }
+        __syncthreads();
+    }
+
+    // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
+#pragma unroll
+    for (int t = 0; t < TB; ++t) {
+        const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int k = kb * 16 + (lane >> 4) * 4 + v;
+            float mm[T2];
+#pragma unroll
+            for (int f = 0; f < T2; ++f) mm[f] = acc[t][f][v];
+            float yy[M * M];
+            output_tile_transform<M>(mm, yy);
+            if (ti.ok && k < g.K)
+                store_tile<M>(y + ((long long)ti.n * g.K + k) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
         }
     }
 }
@@ -321,17 +702,22 @@ hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt,
 }
 
 bool fused_cfg_supported(int m, const FusedCfg &cfg) {
+    if (m != 2 && m != 4 && m != 6) return false;
+    if (cfg.schedule == kSchedSpecialised) return m <= 4;
+    if (cfg.schedule == kSchedShared) return cfg.tb == 1 || (cfg.tb == 2 && m <= 4);
+    if (cfg.schedule != kSchedPerWave) return false;
     if (cfg.waves < 1 || cfg.waves > 4) return false;
     switch (m) {
         case 2: return cfg.nkb == 1 || cfg.nkb == 2 || cfg.nkb == 4;
         case 4: return cfg.nkb == 1 || cfg.nkb == 2;
-        case 6: return cfg.nkb == 1;
-        default: return false;
+        default: return cfg.nkb == 1;
     }
 }
 
 FusedCfg fused_cfg_default(const Geometry &g) {
     FusedCfg c;
+    c.schedule = g.m <= 4 ? kSchedSpecialised : kSchedShared;
+    c.tb = (g.m == 2) ? 2 : 1;
     c.waves = 4;
     switch (g.m) {
         case 2: c.nkb = g.Kb >= 4 ? 4 : (g.Kb >= 2 ? 2 : 1); break;
@@ -339,6 +725,24 @@ FusedCfg fused_cfg_default(const Geometry &g) {
         default: c.nkb = 1; break;
     }
     return c;
+}
+
+template <int M, int TB>
+static void launch_ws_t(const Geometry &g, const float *x, const float *wt, float *y, bool vec,
+                        hipStream_t s) {
+    dim3 block(512);
+    dim3 grid((unsigned)((g.ntiles + 16 * TB - 1) / (16 * TB)), (unsigned)((g.Kb + 3) / 4));
+    hipLaunchKernelGGL((fused_ws_kernel<M, TB>), grid, block, 0, s, x,
+                       reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0);
+}
+
+template <int M, int TB>
+static void launch_shared_t(const Geometry &g, const float *x, const float *wt, float *y,
+                            hipStream_t s) {
+    dim3 block(256);
+    dim3 grid((unsigned)((g.ntiles + 16 * TB - 1) / (16 * TB)), (unsigned)((g.Kb + 3) / 4));
+    hipLaunchKernelGGL((fused_shared_kernel<M, TB>), grid, block, 0, s, x,
+                       reinterpret_cast<const floatx4 *>(wt), y, g);
 }
 
 template <int M, int NKB>
@@ -355,6 +759,31 @@ static void launch_fused_t(const Geometry &g, int waves, const float *x, const f
 hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, const float *wt,
                         float *y, hipStream_t s) {
     if (!fused_cfg_supported(g.m, cfg)) return hipErrorInvalidValue;
+    if (cfg.schedule == kSchedSpecialised) {
+        const uintptr_t ya = reinterpret_cast<uintptr_t>(y);
+        const bool vec = (g.m == 4) ? (g.W % 4 == 0 && ya % 16 == 0) : (g.W % 2 == 0 && ya % 8 == 0);
+        switch (g.m) {
+            case 2: launch_ws_t<2, 2>(g, x, wt, y, vec, s); break;
+            default: launch_ws_t<4, 1>(g, x, wt, y, vec, s); break;
+        }
+        return hipGetLastError();
+    }
+    if (cfg.schedule == kSchedShared) {
+        switch (g.m) {
+            case 2:
+                if (cfg.tb == 2) launch_shared_t<2, 2>(g, x, wt, y, s);
+                else launch_shared_t<2, 1>(g, x, wt, y, s);
+                break;
+            case 4:
+                if (cfg.tb == 2) launch_shared_t<4, 2>(g, x, wt, y, s);
+                else launch_shared_t<4, 1>(g, x, wt, y, s);
+                break;
+            default:
+                launch_shared_t<6, 1>(g, x, wt, y, s);
+                break;
+        }
+        return hipGetLastError();
+    }
     switch (g.m) {
         case 2:
             if (cfg.nkb == 1) launch_fused_t<2, 1>(g, cfg.waves, x, wt, y, s);
@@ -365,11 +794,9 @@ hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, 
             if (cfg.nkb == 1) launch_fused_t<4, 1>(g, cfg.waves, x, wt, y, s);
             else launch_fused_t<4, 2>(g, cfg.waves, x, wt, y, s);
             break;
-        case 6:
+        default:
             launch_fused_t<6, 1>(g, cfg.waves, x, wt, y, s);
             break;
-        default:
-            return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

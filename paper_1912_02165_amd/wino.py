@@ -37,9 +37,12 @@ SIGNATURES = {
 }
 
 
+WINO_SCHED_AUTO, WINO_SCHED_SHARED, WINO_SCHED_PER_WAVE = 0, 1, 2
+
+
 class WinoTuning(ctypes.Structure):
-    _fields_ = [("k_blocks_per_wave", ctypes.c_int), ("waves_per_group", ctypes.c_int),
-                ("reserved0", ctypes.c_int), ("reserved1", ctypes.c_int)]
+    _fields_ = [("schedule", ctypes.c_int), ("k_blocks_per_wave", ctypes.c_int),
+                ("waves_per_group", ctypes.c_int), ("tile_blocks", ctypes.c_int)]
 
 
 class WinoError(RuntimeError):

@@ -73,8 +73,12 @@ def test_bad_algo(lib):
 
 
 def test_bad_tuning(lib):
-    t = wino.WinoTuning(k_blocks_per_wave=3)
+    t = wino.WinoTuning(schedule=wino.WINO_SCHED_PER_WAVE, k_blocks_per_wave=3)
     assert "not built" in _plan_fails(lib, 1, 4, 4, 8, 8, 6, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+    t = wino.WinoTuning(schedule=wino.WINO_SCHED_SHARED, tile_blocks=2)
+    assert "not built" in _plan_fails(lib, 1, 4, 4, 8, 8, 6, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+    t = wino.WinoTuning(schedule=5)
+    assert "not built" in _plan_fails(lib, 1, 4, 4, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
     t = wino.WinoTuning(waves_per_group=-1)
     assert ">= 0" in _plan_fails(lib, 1, 4, 4, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
 

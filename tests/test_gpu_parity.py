@@ -177,8 +177,14 @@ def test_tuning_overrides_agree():
     for m, nkbs in ((2, (1, 2, 4)), (4, (1, 2)), (6, (1,))):
         for nkb in nkbs:
             for waves in (1, 2, 4):
-                y = run_gpu(x, w, m, "fused", {"k_blocks_per_wave": nkb, "waves_per_group": waves})
-                assert_close(y.cpu().numpy(), ref, m, f"F({m}) nkb={nkb} waves={waves}")
+                t = {"schedule": wc.WINO_SCHED_PER_WAVE, "k_blocks_per_wave": nkb,
+                     "waves_per_group": waves}
+                y = run_gpu(x, w, m, "fused", t)
+                assert_close(y.cpu().numpy(), ref, m, f"per-wave F({m}) nkb={nkb} waves={waves}")
+        for tb in ((1, 2) if m <= 4 else (1,)):
+            t = {"schedule": wc.WINO_SCHED_SHARED, "tile_blocks": tb}
+            y = run_gpu(x, w, m, "fused", t)
+            assert_close(y.cpu().numpy(), ref, m, f"shared F({m}) tile_blocks={tb}")
 
 
 def test_bad_pointers_rejected():
