@@ -457,24 +457,156 @@ __device__ __forceinline__ void store_tile(float *__restrict__ yp, const float *
 
 // ---------------------------------------------------------------------------
 // Fused kernel, warp-specialised schedule.  A workgroup of 8 waves is one task of
-// R = 16*TB tiles and 64 output channels.  Waves 4..7 are producers: per stage of
-// CC = 256/R channels each of their lanes loads one (tile, channel) input tile,
-// transforms it (B^T d B) and writes its T^2 values to LDS.  Waves 0..3 are
-// consumers: wave w multiplies the stage's transformed tiles by the transformed
-// kernels of output-channel block w on the matrix cores, with the kernel operands
-// of the next 4-channel step loaded while the current step runs.  Two waves per
-// SIMD (one of each kind) let the producers' vector work run while the matrix
-// cores are busy.  LDS is double-buffered with one barrier per stage; the layout
-// of a buffer is that of fused_shared_kernel.
-template <int M, int TB>
+// R = 16*TB tiles and 64/FS output channels (Sec. 4).
+//
+// Waves 4..7 are producers: per stage of CC = 256/R channels each lane loads one
+// (tile, channel) input tile, transforms it (B^T d B) and writes its T^2 values to
+// LDS; the loads of the next stage are issued before the transform, so their
+// latency hides behind it and behind the barrier.
+//
+// Waves 0..3 are consumers on the matrix cores.  With FS = 1, wave w owns output
+// block w and all T^2 frequencies.  With FS = 2 (F(6), whose 64 frequencies would
+// need 256 accumulators), waves 2b and 2b+1 share output block b and each owns
+// half of the transform-domain rows; by linearity of the output transform each
+// inverse-transforms its own rows and the two partial tiles are added through
+// LDS, reusing the input-tile buffers once the channel loop is over (the result
+// matrices taking the place of dead left-hand matrices, as in Sec. 4.2).  The
+// kernel operands of the next 4-channel step are loaded while the current step
+// runs.
+//
+// Two waves per SIMD (a producer and a consumer) let the producers' vector work
+// overlap the matrix cores.  LDS holds two stage buffers with one barrier per
+// stage; the layout of a buffer is that of fused_shared_kernel.
+
+// Transform-domain rows owned by frequency group G of FS (bit i = row i).
+template <int M, int FS, int G>
+constexpr unsigned group_rows() {
+    if constexpr (FS == 1) return (1u << (M + 2)) - 1u;
+    else return G == 0 ? 0x87u : 0x78u;  // F(6): rows {0,1,2,7} and {3,4,5,6}
+}
+
+// Global float4 frequency index of the group's lf-th float4 (T = 8: a row is two float4s).
+template <int M, int FS, int G>
+constexpr int group_f4(int lf) {
+    if constexpr (FS == 1) return lf;
+    else {
+        constexpr unsigned rows = group_rows<M, FS, G>();
+        int seen = 0;
+        for (int i = 0; i < M + 2; ++i)
+            if ((rows >> i) & 1u) {
+                if (lf < seen + 2) return 2 * i + (lf - seen);
+                seen += 2;
+            }
+        return -1;
+    }
+}
+
+template <int M, int TB, int FS, int G>
+__device__ __forceinline__ void ws_consume(floatx4 *__restrict__ lds, const floatx4 *__restrict__ wk,
+                                           float *__restrict__ y, const Geometry &g, int tile0,
+                                           int kb, int kbl, int lane, int stages, int vec) {
+    constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
+    constexpr int R = 16 * TB, CC = 256 / R, SS = CC / 4, BUF = F4 * CC * R;
+    constexpr int NF4 = F4 / FS;
+    static_assert(FS == 1 || T == 8, "frequency split is built for F(6) only");
+    const long long HW = (long long)g.H * g.W;
+
+    floatx4 acc[TB][NF4 * 4];
+#pragma unroll
+    for (int t = 0; t < TB; ++t)
+#pragma unroll
+        for (int f = 0; f < NF4 * 4; ++f) acc[t][f] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    floatx4 aw[NF4];
+#pragma unroll
+    for (int lf = 0; lf < NF4; ++lf) aw[lf] = wk[group_f4<M, FS, G>(lf) * 64];
+    __syncthreads();  // stage 0 is in LDS
+    for (int j = 0; j < stages; ++j) {
+        const floatx4 *cur = lds + (j & 1) * BUF;
+#pragma unroll
+        for (int s = 0; s < SS; ++s) {
+            const int cs = j * SS + s;
+            if (cs < g.Cs) {
+                floatx4 an[NF4];
+                const int cn = cs + 1 < g.Cs ? cs + 1 : cs;
+#pragma unroll
+                for (int lf = 0; lf < NF4; ++lf)
+                    an[lf] = wk[((long long)cn * F4 + group_f4<M, FS, G>(lf)) * 64];
+                const floatx4 *bp = cur + (4 * s + (lane >> 4)) * R + (lane & 15);
+#pragma unroll
+                for (int lf = 0; lf < NF4; ++lf) {
+#pragma unroll
+                    for (int t = 0; t < TB; ++t) {
+                        const floatx4 b = bp[group_f4<M, FS, G>(lf) * CC * R + t * 16];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            acc[t][4 * lf + q] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                aw[lf][q], b[q], acc[t][4 * lf + q], 0, 0, 0);
+                    }
+                }
+#pragma unroll
+                for (int lf = 0; lf < NF4; ++lf) aw[lf] = an[lf];
+            }
+        }
+        __syncthreads();
+    }
+
+    // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
+    constexpr unsigned ROWS = group_rows<M, FS, G>();
+    float *part = reinterpret_cast<float *>(lds);  // FS = 2: partial tiles of group 1
+    if constexpr (G == 1) {
+#pragma unroll
+        for (int t = 0; t < TB; ++t)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                float mm[T2];
+#pragma unroll
+                for (int lf = 0; lf < NF4; ++lf)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) mm[group_f4<M, FS, G>(lf) * 4 + q] = acc[t][4 * lf + q][v];
+                float yy[M * M];
+                output_tile_transform_rows<M, ROWS>(mm, yy);
+                float *dst = part + (((long long)(kbl * TB + t) * 4 + v) * M * M) * 64 + lane;
+#pragma unroll
+                for (int e = 0; e < M * M; ++e) dst[e * 64] = yy[e];
+            }
+        __syncthreads();
+        return;
+    }
+    if constexpr (FS == 2) __syncthreads();
+#pragma unroll
+    for (int t = 0; t < TB; ++t) {
+        const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int k = kb * 16 + (lane >> 4) * 4 + v;
+            float mm[T2];
+#pragma unroll
+            for (int lf = 0; lf < NF4; ++lf)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) mm[group_f4<M, FS, G>(lf) * 4 + q] = acc[t][4 * lf + q][v];
+            float yy[M * M];
+            output_tile_transform_rows<M, ROWS>(mm, yy);
+            if constexpr (FS == 2) {
+                const float *src = part + (((long long)(kbl * TB + t) * 4 + v) * M * M) * 64 + lane;
+#pragma unroll
+                for (int e = 0; e < M * M; ++e) yy[e] += src[e * 64];
+            }
+            if (ti.ok && k < g.K)
+                store_tile<M>(y + ((long long)ti.n * g.K + k) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
+        }
+    }
+}
+
+template <int M, int TB, int FS>
 __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__ x,
                                                        const floatx4 *__restrict__ wt,
                                                        float *__restrict__ y, Geometry g, int vec) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB;
     constexpr int CC = 256 / R;
-    constexpr int SS = CC / 4;
     constexpr int BUF = F4 * CC * R;
+    constexpr int KBW = 4 / FS;  // output blocks per workgroup
     __shared__ floatx4 lds[2 * BUF];
 
     const int tid = threadIdx.x;
@@ -496,86 +628,44 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         ld.init(g, decode_tile(g, tile0 + tr), cl);
         const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
         const bool ctail = (g.C % CC) != 0;
-        for (int j = -1; j < stages; ++j) {
-            const int st = j + 1;  // stage produced in this round
+        auto load_stage = [&](int st, float *d) {
+            const long long cbase = (long long)st * CC * HW;
+            ld.load(make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4)), d);
+        };
+        // round st: prefetch stage st+1, transform stage st into buffer st&1, barrier
+        auto round = [&](int st, float *dcur, float *dnext) {
+            if (st + 1 < stages) load_stage(st + 1, dnext);
             if (st < stages) {
-                float d[T2];
-                const long long cbase = (long long)st * CC * HW;
-                ld.load(make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4)), d);
-                float u[T2];
-                input_tile_transform<M>(d, u);
-                if (ctail && st == stages - 1 && st * CC + cl >= g.C) {
-#pragma unroll
-                    for (int f = 0; f < T2; ++f) u[f] = 0.0f;
-                }
-                floatx4 *buf = lds + (st & 1) * BUF;
-#pragma unroll
-                for (int f4 = 0; f4 < F4; ++f4)
-                    buf[(f4 * CC + cl) * R + tr] =
-                        floatx4{u[4 * f4], u[4 * f4 + 1], u[4 * f4 + 2], u[4 * f4 + 3]};
+                // channels past C (last stage only, when C % CC != 0) store zeros
+                const bool zero = ctail && st == stages - 1 && st * CC + cl >= g.C;
+                floatx4 *buf = lds + (st & 1) * BUF + cl * R + tr;
+                input_tile_transform_emit<M>(dcur, [&](int f4, float a, float b, float c, float e) {
+                    buf[f4 * CC * R] = zero ? floatx4{0.f, 0.f, 0.f, 0.f} : floatx4{a, b, c, e};
+                });
             }
             __syncthreads();
+        };
+        float d0[T2], d1[T2];
+        load_stage(0, d0);
+        int st = 0;
+        for (; st + 1 <= stages; st += 2) {
+            round(st, d0, d1);
+            round(st + 1, d1, d0);
         }
+        if (st <= stages) round(st, d0, d1);
+        if constexpr (FS == 2) __syncthreads();  // matches the consumers' combine barrier
         return;
     }
 
-    // ---------------- consumer: per-frequency products on the matrix cores ----------------
-    const int kb = kgrp * 4 + wave;
+    // ---------------- consumers ----------------
+    const int kbl = wave / FS;
+    const int kb = kgrp * KBW + kbl;
     const floatx4 *wk = wt + (long long)kb * g.Cs * F4 * 64 + lane;
-    floatx4 acc[TB][T2];
-#pragma unroll
-    for (int t = 0; t < TB; ++t)
-#pragma unroll
-        for (int f = 0; f < T2; ++f) acc[t][f] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    floatx4 aw[F4];
-#pragma unroll
-    for (int f4 = 0; f4 < F4; ++f4) aw[f4] = wk[f4 * 64];
-    __syncthreads();  // stage 0 is in LDS
-    for (int j = 0; j < stages; ++j) {
-        const floatx4 *cur = lds + (j & 1) * BUF;
-#pragma unroll
-        for (int s = 0; s < SS; ++s) {
-            const int cs = j * SS + s;
-            if (cs < g.Cs) {
-                floatx4 an[F4];
-                const int cn = cs + 1 < g.Cs ? cs + 1 : cs;
-#pragma unroll
-                for (int f4 = 0; f4 < F4; ++f4) an[f4] = wk[((long long)cn * F4 + f4) * 64];
-                const floatx4 *bp = cur + (4 * s + (lane >> 4)) * R + (lane & 15);
-#pragma unroll
-                for (int f4 = 0; f4 < F4; ++f4) {
-#pragma unroll
-                    for (int t = 0; t < TB; ++t) {
-                        const floatx4 b = bp[f4 * CC * R + t * 16];
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            acc[t][4 * f4 + q] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                aw[f4][q], b[q], acc[t][4 * f4 + q], 0, 0, 0);
-                    }
-                }
-#pragma unroll
-                for (int f4 = 0; f4 < F4; ++f4) aw[f4] = an[f4];
-            }
-        }
-        __syncthreads();
-    }
-
-    // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
-#pragma unroll
-    for (int t = 0; t < TB; ++t) {
-        const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int k = kb * 16 + (lane >> 4) * 4 + v;
-            float mm[T2];
-#pragma unroll
-            for (int f = 0; f < T2; ++f) mm[f] = acc[t][f][v];
-            float yy[M * M];
-            output_tile_transform<M>(mm, yy);
-            if (ti.ok && k < g.K)
-                store_tile<M>(y + ((long long)ti.n * g.K + k) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
-        }
+    if constexpr (FS == 1) {
+        ws_consume<M, TB, 1, 0>(lds, wk, y, g, tile0, kb, kbl, lane, stages, vec);
+    } else {
+        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, wk, y, g, tile0, kb, kbl, lane, stages, vec);
+        else ws_consume<M, TB, FS, 1>(lds, wk, y, g, tile0, kb, kbl, lane, stages, vec);
     }
 }
 
@@ -703,7 +793,7 @@ hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt,
 
 bool fused_cfg_supported(int m, const FusedCfg &cfg) {
     if (m != 2 && m != 4 && m != 6) return false;
-    if (cfg.schedule == kSchedSpecialised) return m <= 4;
+    if (cfg.schedule == kSchedSpecialised) return true;
     if (cfg.schedule == kSchedShared) return cfg.tb == 1 || (cfg.tb == 2 && m <= 4);
     if (cfg.schedule != kSchedPerWave) return false;
     if (cfg.waves < 1 || cfg.waves > 4) return false;
@@ -716,7 +806,7 @@ bool fused_cfg_supported(int m, const FusedCfg &cfg) {
 
 FusedCfg fused_cfg_default(const Geometry &g) {
     FusedCfg c;
-    c.schedule = g.m <= 4 ? kSchedSpecialised : kSchedShared;
+    c.schedule = kSchedSpecialised;
     c.tb = (g.m == 2) ? 2 : 1;
     c.waves = 4;
     switch (g.m) {
@@ -727,12 +817,13 @@ FusedCfg fused_cfg_default(const Geometry &g) {
     return c;
 }
 
-template <int M, int TB>
+template <int M, int TB, int FS>
 static void launch_ws_t(const Geometry &g, const float *x, const float *wt, float *y, bool vec,
                         hipStream_t s) {
+    constexpr int KBW = 4 / FS;
     dim3 block(512);
-    dim3 grid((unsigned)((g.ntiles + 16 * TB - 1) / (16 * TB)), (unsigned)((g.Kb + 3) / 4));
-    hipLaunchKernelGGL((fused_ws_kernel<M, TB>), grid, block, 0, s, x,
+    dim3 grid((unsigned)((g.ntiles + 16 * TB - 1) / (16 * TB)), (unsigned)((g.Kb + KBW - 1) / KBW));
+    hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS>), grid, block, 0, s, x,
                        reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0);
 }
 
@@ -763,8 +854,9 @@ hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, 
         const uintptr_t ya = reinterpret_cast<uintptr_t>(y);
         const bool vec = (g.m == 4) ? (g.W % 4 == 0 && ya % 16 == 0) : (g.W % 2 == 0 && ya % 8 == 0);
         switch (g.m) {
-            case 2: launch_ws_t<2, 2>(g, x, wt, y, vec, s); break;
-            default: launch_ws_t<4, 1>(g, x, wt, y, vec, s); break;
+            case 2: launch_ws_t<2, 2, 1>(g, x, wt, y, vec, s); break;
+            case 4: launch_ws_t<4, 1, 1>(g, x, wt, y, vec, s); break;
+            default: launch_ws_t<6, 1, 2>(g, x, wt, y, vec, s); break;
         }
         return hipGetLastError();
     }

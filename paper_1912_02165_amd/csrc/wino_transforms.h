@@ -200,6 +200,25 @@ __device__ __forceinline__ void input_tile_transform(const float *d, float *u) {
     for (int i = 0; i < T; ++i) bt_1d<M, 1, 1>(tmp + i * T, u + i * T);  // rows: (B^T d) B
 }
 
+// U = B^T d B as above, handing each finished group of four consecutive
+// frequencies to emit(f4, u0, u1, u2, u3) as soon as its rows are done, so the
+// whole T^2 result never has to be live at once.
+template <int M, class Emit>
+__device__ __forceinline__ void input_tile_transform_emit(const float *d, Emit &&emit) {
+    constexpr int T = M + 2;
+    float tmp[T * T];
+#pragma unroll
+    for (int b = 0; b < T; ++b) bt_1d<M, T, T>(d + b, tmp + b);       // columns: B^T d
+    float u[T * T];
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+        bt_1d<M, 1, 1>(tmp + i * T, u + i * T);                        // row i of (B^T d) B
+#pragma unroll
+        for (int f4 = (i * T) / 4; f4 < ((i + 1) * T) / 4; ++f4)      // float4s completed by row i
+            emit(f4, u[4 * f4], u[4 * f4 + 1], u[4 * f4 + 2], u[4 * f4 + 3]);
+    }
+}
+
 // Y = A^T Mm A for a T x T tile Mm (row-major); Y is M x M row-major.
 template <int M>
 __device__ __forceinline__ void output_tile_transform(const float *mm, float *yv) {
@@ -209,6 +228,58 @@ __device__ __forceinline__ void output_tile_transform(const float *mm, float *yv
     for (int b = 0; b < T; ++b) at_1d<M, T, T>(mm + b, tmp + b);      // columns: A^T Mm
 #pragma unroll
     for (int i = 0; i < M; ++i) at_1d<M, 1, 1>(tmp + i * T, yv + i * M);  // rows: (A^T Mm) A
+}
+
+// out[i*SO] = sum_{j in ROWS} A^T[i][j] in[j*SI]: A^T applied to a vector whose
+// entries outside the bit set ROWS are zero (a +-p pair is either fully in ROWS
+// or fully out).  Used when a tile's frequencies are split between waves: by
+// linearity each wave inverse-transforms its own rows and the partial outputs
+// add up to the full one.
+template <int M, int SI, int SO, unsigned ROWS>
+__device__ __forceinline__ void at_1d_rows(const float *in, float *out) {
+    constexpr Tables<M> tb{};
+    constexpr int T = M + 2;
+    constexpr int NP = (T - 2) / 2;
+    float s[NP], d[NP];
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+        if ((ROWS >> (1 + 2 * q)) & 1u) {
+            s[q] = in[(1 + 2 * q) * SI] + in[(2 + 2 * q) * SI];
+            d[q] = in[(1 + 2 * q) * SI] - in[(2 + 2 * q) * SI];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+        float acc = 0.f;
+        bool first = true;
+        if (ROWS & 1u) mac(acc, first, tb.at[i][0], in[0]);
+#pragma unroll
+        for (int q = 0; q < NP; ++q)
+            if ((ROWS >> (1 + 2 * q)) & 1u) mac(acc, first, tb.at[i][1 + 2 * q], (i % 2 == 0) ? s[q] : d[q]);
+        if ((ROWS >> (T - 1)) & 1u) mac(acc, first, tb.at[i][T - 1], in[(T - 1) * SI]);
+        out[i * SO] = first ? 0.0f : acc;
+    }
+}
+
+template <int M, unsigned ROWS>
+constexpr bool rows_pair_closed() {
+    constexpr int T = M + 2;
+    for (int j = 1; j + 1 < T - 1; j += 2)
+        if (((ROWS >> j) & 1u) != ((ROWS >> (j + 1)) & 1u)) return false;
+    return true;
+}
+
+// Partial output tile: Y_part = A^T Mm_rows A, where only the transform-domain
+// rows in ROWS of Mm (row-major T x T) are used.
+template <int M, unsigned ROWS>
+__device__ __forceinline__ void output_tile_transform_rows(const float *mm, float *yv) {
+    static_assert(rows_pair_closed<M, ROWS>(), "row set must hold whole +-p pairs");
+    constexpr int T = M + 2;
+    float tmp[M * T];
+#pragma unroll
+    for (int b = 0; b < T; ++b) at_1d_rows<M, T, T, ROWS>(mm + b, tmp + b);
+#pragma unroll
+    for (int i = 0; i < M; ++i) at_1d<M, 1, 1>(tmp + i * T, yv + i * M);
 }
 
 // W' = G g G^T for a 3 x 3 kernel g (row-major); W' is T x T row-major.
