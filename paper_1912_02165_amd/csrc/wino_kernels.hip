@@ -11,6 +11,8 @@
 // B operand for all T^2 frequencies from one input tile held in registers, and
 // after the channel loop it holds, for its tile, all T^2 frequencies of four
 // output channels, so the output transform also runs in registers.
+#include <type_traits>
+
 #include "wino_internal.h"
 #include "wino_transforms.h"
 
@@ -121,10 +123,26 @@ __global__ void __launch_bounds__(256) weight_transform_kernel(const float *__re
 // the implicit zero padding of Sec. 2.1 with unconditional loads: offsets of rows
 // or columns outside the image are pushed to >= 2^31 (x is below 2^31 bytes) with
 // a saturating add.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float *base, unsigned bytes) {
-    // dword3 = 0x00020000: 32-bit data format, as raw buffer loads on gfx9 expect
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), (short)0, (int)bytes,
-                                             0x00020000);
+typedef int int32x4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+
+// Raw buffer loads, called through the LLVM intrinsics with an explicit 4-dword
+// resource (base address, size in bytes, 32-bit data format).
+__device__ float buffer_load_f32(int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.load.f32");
+__device__ floatx2 buffer_load_f32x2(int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.load.v2f32");
+__device__ floatx4 buffer_load_f32x4(int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.load.v4f32");
+
+__device__ __forceinline__ int32x4 make_rsrc(const float *base, unsigned bytes) {
+    const unsigned long long p = reinterpret_cast<unsigned long long>(base);
+    int32x4 r;
+    r[0] = (int)(unsigned)(p & 0xffffffffull);
+    r[1] = (int)(unsigned)((p >> 32) & 0xffffull);  // stride 0: raw buffer
+    r[2] = (int)bytes;                                 // range-checked size
+    r[3] = 0x00020000;                                 // 32-bit data format
+    return r;
 }
 
 constexpr unsigned kOutside = 0x80000000u;
@@ -171,12 +189,91 @@ struct BufTile {
         else return __builtin_elementwise_add_sat(roff[a], coff[b]);
     }
 
-    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, float *d) const {
+    __device__ __forceinline__ void load(int32x4 r, float *d) const {
 #pragma unroll
         for (int a = 0; a < T; ++a)
 #pragma unroll
             for (int b = 0; b < T; ++b)
-                d[a * T + b] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, offset(a, b), 0, 0));
+                d[a * T + b] = buffer_load_f32(r, offset(a, b), 0, 0);
+    }
+};
+
+// Row-vector loads of input tiles.  Lanes l and l+1 of a 16-lane DPP row hold
+// horizontally adjacent tiles of the same channel (tiles are numbered along
+// rows), and the T = m + 2 columns of a tile's row are its own m columns plus one
+// halo column on each side, which are the neighbours' own edge columns.  So each
+// lane loads only its own m columns of a row with one vector load and takes the
+// halo columns from lanes l-1 and l+1 with DPP row shifts.  A tile in the first
+// (last) column of tiles has zero padding on its left (right); a lane at the
+// edge of a 16-lane row whose neighbour tile is in another group fetches that
+// one column itself.  The vector loads need rows aligned to the vector width
+// (checked on the host).
+__device__ __forceinline__ float dpp_from_left(float v) {   // lane l gets lane l-1 (0 at row start)
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                                 0x111, 0xf, 0xf, true));
+}
+__device__ __forceinline__ float dpp_from_right(float v) {  // lane l gets lane l+1 (0 at row end)
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                                 0x101, 0xf, 0xf, true));
+}
+
+template <int M>
+struct RowTile {
+    static constexpr int T = M + 2;
+    unsigned roff[T];   // byte offset of column 0 of input row a (>= 2^31 if outside)
+    unsigned own;       // byte offset of the tile's first own column, tx*M*4
+    bool first, last;   // tile in the first / last column of tiles: halo is padding
+    bool fetch_l, fetch_r;
+    unsigned ownok;     // bit j: own column j lies inside the image
+
+    __device__ __forceinline__ void init(const Geometry &g, const TileIdx &t, int lane_c, int lane16) {
+        const unsigned base = (unsigned)(((long long)t.n * g.C + lane_c) * g.H * g.W) * 4u;
+#pragma unroll
+        for (int a = 0; a < T; ++a) {
+            const int h = t.ty * M - 1 + a;
+            roff[a] = (t.ok && h >= 0 && h < g.H) ? base + (unsigned)(h * g.W) * 4u : kOutside;
+        }
+        own = (unsigned)(t.tx * M) * 4u;
+        first = t.tx == 0;
+        last = t.tx == g.TW - 1;
+        fetch_l = lane16 == 0 && !first;
+        fetch_r = lane16 == 15 && !last;
+        ownok = 0u;
+#pragma unroll
+        for (int j = 0; j < M; ++j)
+            if (t.tx * M + j < g.W) ownok |= 1u << j;
+    }
+
+    __device__ __forceinline__ void load(int32x4 r, float *d, bool maskcols) const {
+#pragma unroll
+        for (int a = 0; a < T; ++a) {
+            const unsigned ro = roff[a];
+            // Own columns with one vector load (two 8-byte loads and one more for
+            // m = 6).  ro is below 2^31 or exactly 2^31 and own + 4*M is below
+            // 2^31, so the offsets never wrap.
+            const unsigned base = ro + own;
+            float v[M];
+            if constexpr (M == 4) {
+                const floatx4 q = buffer_load_f32x4(r, base, 0, 0);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) v[j] = q[j];
+            } else {
+#pragma unroll
+                for (int j = 0; j < M; j += 2) {
+                    const floatx2 q = buffer_load_f32x2(r, base + 4u * j, 0, 0);
+                    v[j] = q[0];
+                    v[j + 1] = q[1];
+                }
+            }
+            const float lf = buffer_load_f32(r, fetch_l ? base - 4u : kOutside, 0, 0);
+            const float rt = buffer_load_f32(r, fetch_r ? base + 4u * M : kOutside, 0, 0);
+            const float ln = dpp_from_left(v[M - 1]);
+            const float rn = dpp_from_right(v[0]);
+            d[a * T] = first ? 0.0f : (fetch_l ? lf : ln);
+#pragma unroll
+            for (int j = 0; j < M; ++j) d[a * T + 1 + j] = (maskcols && !((ownok >> j) & 1u)) ? 0.0f : v[j];
+            d[a * T + T - 1] = last ? 0.0f : (fetch_r ? rt : rn);
+        }
     }
 };
 
@@ -442,8 +539,7 @@ __device__ __forceinline__ void store_tile(float *__restrict__ yp, const float *
                 *reinterpret_cast<floatx4 *>(row) =
                     floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]};
             } else {
-                typedef float floatx2 __attribute__((ext_vector_type(2)));
-#pragma unroll
+                #pragma unroll
                 for (int jj = 0; jj < M; jj += 2)
                     *reinterpret_cast<floatx2 *>(row + jj) = floatx2{yy[i * M + jj], yy[i * M + jj + 1]};
             }
@@ -598,7 +694,7 @@ __device__ __forceinline__ void ws_consume(floatx4 *__restrict__ lds, const floa
     }
 }
 
-template <int M, int TB, int FS>
+template <int M, int TB, int FS, bool VX>
 __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__ x,
                                                        const floatx4 *__restrict__ wt,
                                                        float *__restrict__ y, Geometry g, int vec) {
@@ -624,13 +720,19 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         const int pt = tid - 256;
         const int tr = pt % R;
         const int cl = pt / R;
-        BufTile<M, (M <= 2)> ld;
-        ld.init(g, decode_tile(g, tile0 + tr), cl);
+        // VX: row-vector loads with DPP halo exchange; otherwise one load per element
+        using Loader = typename std::conditional<VX, RowTile<M>, BufTile<M, (M <= 2)>>::type;
+        Loader ld;
+        if constexpr (VX) ld.init(g, decode_tile(g, tile0 + tr), cl, lane & 15);
+        else ld.init(g, decode_tile(g, tile0 + tr), cl);
+        const bool maskcols = (g.W % M) != 0;
         const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
         const bool ctail = (g.C % CC) != 0;
         auto load_stage = [&](int st, float *d) {
             const long long cbase = (long long)st * CC * HW;
-            ld.load(make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4)), d);
+            const int32x4 rs = make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4));
+            if constexpr (VX) ld.load(rs, d, maskcols);
+            else ld.load(rs, d);
         };
         // round st: prefetch stage st+1, transform stage st into buffer st&1, barrier
         auto round = [&](int st, float *dcur, float *dnext) {
@@ -823,8 +925,15 @@ static void launch_ws_t(const Geometry &g, const float *x, const float *wt, floa
     constexpr int KBW = 4 / FS;
     dim3 block(512);
     dim3 grid((unsigned)((g.ntiles + 16 * TB - 1) / (16 * TB)), (unsigned)((g.Kb + KBW - 1) / KBW));
-    hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS>), grid, block, 0, s, x,
-                       reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0);
+    // row-vector input loads need every row start aligned to the vector width
+    const unsigned vw = (M == 4) ? 16u : 8u;
+    const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
+    if (vx)
+        hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, true>), grid, block, 0, s, x,
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0);
+    else
+        hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, false>), grid, block, 0, s, x,
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0);
 }
 
 template <int M, int TB>

@@ -211,3 +211,19 @@ def test_bad_pointers_rejected():
                       ptr.value)
     finally:
         hip.hipFree(ptr)
+
+
+@pytest.mark.parametrize("m", (2, 4, 6))
+def test_unaligned_input_pointer(m):
+    """x starting 4 bytes past an aligned address takes the per-element load path."""
+    N, C, K, H, W = 2, 9, 20, 16, 24
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=9 + m)
+    buf = torch.zeros(x.size + 1, device="cuda")
+    buf[1:] = torch.from_numpy(x.reshape(-1)).cuda()
+    xd = buf[1:].view(N, C, H, W)
+    assert xd.data_ptr() % 16 == 4
+    y = torch.empty((N, K, H, W), device="cuda")
+    with wc.Plan(N, C, K, H, W, m) as p:
+        p.run(xd, torch.from_numpy(w).cuda(), y)
+        torch.cuda.synchronize()
+    assert_close(y.cpu().numpy(), direct_conv(x, w), m, f"unaligned x F({m})")
