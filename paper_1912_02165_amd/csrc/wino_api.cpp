@@ -237,6 +237,15 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         set_err("host allocation failed");
         return nullptr;
     }
+    {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus < 1) {
+            (void)hipGetLastError();
+            cus = 256;
+        }
+        cfg.num_cus = cus;
+    }
     p->g = g;
     p->algo = algo;
     p->fcfg = cfg;

@@ -27,6 +27,7 @@ struct FusedCfg {
     int tb;        // shared: tile blocks of 16 per workgroup
     int nkb;       // per-wave: 16-channel output blocks per wave
     int waves;     // per-wave: waves per workgroup (each owns 16 tiles)
+    int num_cus;   // compute units of the device (persistent grid size)
 };
 
 // Kernel transform: w (K x C x 3 x 3) -> wt in matrix-core operand order.

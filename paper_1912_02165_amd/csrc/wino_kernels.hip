@@ -581,139 +581,158 @@ constexpr unsigned group_rows() {
     else return G == 0 ? 0x87u : 0x78u;  // F(6): rows {0,1,2,7} and {3,4,5,6}
 }
 
-// Global float4 frequency index of the group's lf-th float4 (T = 8: a row is two float4s).
+// Global float4 frequency indices of the group's float4s, as a compile-time
+// table (T = 8: a transform-domain row is two float4s).
 template <int M, int FS, int G>
-constexpr int group_f4(int lf) {
-    if constexpr (FS == 1) return lf;
-    else {
+struct GroupF4 {
+    static constexpr int N = (M + 2) * (M + 2) / 4 / FS;
+    int f4[N];
+    constexpr GroupF4() : f4{} {
         constexpr unsigned rows = group_rows<M, FS, G>();
-        int seen = 0;
-        for (int i = 0; i < M + 2; ++i)
-            if ((rows >> i) & 1u) {
-                if (lf < seen + 2) return 2 * i + (lf - seen);
-                seen += 2;
-            }
-        return -1;
+        if (FS == 1) {
+            for (int i = 0; i < N; ++i) f4[i] = i;
+        } else {
+            int n = 0;
+            for (int i = 0; i < M + 2; ++i)
+                if ((rows >> i) & 1u) {
+                    f4[n++] = 2 * i;
+                    f4[n++] = 2 * i + 1;
+                }
+        }
     }
-}
+};
 
+// Number of barriers a frequency-split (FS = 2) epilogue adds: the partial output
+// tiles of the two waves of a block pair are combined one output channel of the
+// four (v) at a time through a small LDS slot, with a barrier after the write and
+// one after the read.
+template <int FS>
+constexpr int combine_barriers() { return FS == 1 ? 0 : 8; }
+
+// Consumer of the persistent warp-specialised kernel: items it0 .. it1-1, each
+// one (tile group, output-channel group) pair, as one continuous sequence of
+// stages shared with the producers.
 template <int M, int TB, int FS, int G>
-__device__ __forceinline__ void ws_consume(floatx4 *__restrict__ lds, const floatx4 *__restrict__ wk,
-                                           float *__restrict__ y, const Geometry &g, int tile0,
-                                           int kb, int kbl, int lane, int stages, int vec) {
+__device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb,  // shared memory, written by other waves
+                                           const floatx4 *__restrict__ wt, float *__restrict__ y,
+                                           const Geometry &g, int it0, int it1, int n_tgroups,
+                                           int kbl, int lane, int stages, int vec) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB, CC = 256 / R, SS = CC / 4, BUF = F4 * CC * R;
     constexpr int NF4 = F4 / FS;
+    constexpr int KBW = 4 / FS;
+    constexpr unsigned ROWS = group_rows<M, FS, G>();
     static_assert(FS == 1 || T == 8, "frequency split is built for F(6) only");
+    constexpr GroupF4<M, FS, G> gm{};
     const long long HW = (long long)g.H * g.W;
 
-    floatx4 acc[TB][NF4 * 4];
-#pragma unroll
-    for (int t = 0; t < TB; ++t)
-#pragma unroll
-        for (int f = 0; f < NF4 * 4; ++f) acc[t][f] = floatx4{0.f, 0.f, 0.f, 0.f};
+    int q = 0;  // position in the stage sequence (selects the LDS buffer)
+    __syncthreads();  // the first stage is in LDS
+    for (int it = it0; it < it1; ++it) {
+        const int tile0 = (it % n_tgroups) * R;
+        const int kb = (it / n_tgroups) * KBW + kbl;
+        const floatx4 *wk = wt + (long long)kb * g.Cs * F4 * 64 + lane;
 
-    floatx4 aw[NF4];
-#pragma unroll
-    for (int lf = 0; lf < NF4; ++lf) aw[lf] = wk[group_f4<M, FS, G>(lf) * 64];
-    __syncthreads();  // stage 0 is in LDS
-    for (int j = 0; j < stages; ++j) {
-        const floatx4 *cur = lds + (j & 1) * BUF;
-#pragma unroll
-        for (int s = 0; s < SS; ++s) {
-            const int cs = j * SS + s;
-            if (cs < g.Cs) {
-                floatx4 an[NF4];
-                const int cn = cs + 1 < g.Cs ? cs + 1 : cs;
-#pragma unroll
-                for (int lf = 0; lf < NF4; ++lf)
-                    an[lf] = wk[((long long)cn * F4 + group_f4<M, FS, G>(lf)) * 64];
-                const floatx4 *bp = cur + (4 * s + (lane >> 4)) * R + (lane & 15);
-#pragma unroll
-                for (int lf = 0; lf < NF4; ++lf) {
-#pragma unroll
-                    for (int t = 0; t < TB; ++t) {
-                        const floatx4 b = bp[group_f4<M, FS, G>(lf) * CC * R + t * 16];
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            acc[t][4 * lf + q] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                aw[lf][q], b[q], acc[t][4 * lf + q], 0, 0, 0);
-                    }
-                }
-#pragma unroll
-                for (int lf = 0; lf < NF4; ++lf) aw[lf] = an[lf];
-            }
-        }
-        __syncthreads();
-    }
-
-    // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
-    constexpr unsigned ROWS = group_rows<M, FS, G>();
-    float *part = reinterpret_cast<float *>(lds);  // FS = 2: partial tiles of group 1
-    if constexpr (G == 1) {
+        floatx4 acc[TB][NF4 * 4];
 #pragma unroll
         for (int t = 0; t < TB; ++t)
 #pragma unroll
+            for (int f = 0; f < NF4 * 4; ++f) acc[t][f] = floatx4{0.f, 0.f, 0.f, 0.f};
+        floatx4 aw[NF4];
+#pragma unroll
+        for (int lf = 0; lf < NF4; ++lf) aw[lf] = wk[gm.f4[lf] * 64];
+
+        for (int j = 0; j < stages; ++j, ++q) {
+            const floatx4 *cur = lds + (q & 1) * BUF;
+#pragma unroll
+            for (int s = 0; s < SS; ++s) {
+                const int cs = j * SS + s;
+                if (cs < g.Cs) {
+                    floatx4 an[NF4];
+                    const int cn = cs + 1 < g.Cs ? cs + 1 : cs;
+#pragma unroll
+                    for (int lf = 0; lf < NF4; ++lf)
+                        an[lf] = wk[((long long)cn * F4 + gm.f4[lf]) * 64];
+                    const floatx4 *bp = cur + (4 * s + (lane >> 4)) * R + (lane & 15);
+#pragma unroll
+                    for (int lf = 0; lf < NF4; ++lf) {
+#pragma unroll
+                        for (int t = 0; t < TB; ++t) {
+                            const floatx4 b = bp[gm.f4[lf] * CC * R + t * 16];
+#pragma unroll
+                            for (int qq = 0; qq < 4; ++qq)
+                                acc[t][4 * lf + qq] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                    aw[lf][qq], b[qq], acc[t][4 * lf + qq], 0, 0, 0);
+                        }
+                    }
+#pragma unroll
+                    for (int lf = 0; lf < NF4; ++lf) aw[lf] = an[lf];
+                }
+            }
+            __syncthreads();
+        }
+
+        // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
+#pragma unroll
+        for (int t = 0; t < TB; ++t) {
+            const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
+#pragma unroll
             for (int v = 0; v < 4; ++v) {
+                const int k = kb * 16 + (lane >> 4) * 4 + v;
                 float mm[T2];
 #pragma unroll
                 for (int lf = 0; lf < NF4; ++lf)
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) mm[group_f4<M, FS, G>(lf) * 4 + q] = acc[t][4 * lf + q][v];
+                    for (int qq = 0; qq < 4; ++qq) mm[gm.f4[lf] * 4 + qq] = acc[t][4 * lf + qq][v];
                 float yy[M * M];
                 output_tile_transform_rows<M, ROWS>(mm, yy);
-                float *dst = part + (((long long)(kbl * TB + t) * 4 + v) * M * M) * 64 + lane;
+                if constexpr (FS == 2) {
+                    float *slot = comb + (long long)kbl * M * M * 64 + lane;
+                    if constexpr (G == 1) {
 #pragma unroll
-                for (int e = 0; e < M * M; ++e) dst[e * 64] = yy[e];
+                        for (int e = 0; e < M * M; ++e) slot[e * 64] = yy[e];
+                    }
+                    __syncthreads();
+                    if constexpr (G == 0) {
+#pragma unroll
+                        for (int e = 0; e < M * M; ++e) yy[e] += slot[e * 64];
+                    }
+                    __syncthreads();
+                }
+                if (G == 0 && ti.ok && k < g.K)
+                    store_tile<M>(y + ((long long)ti.n * g.K + k) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
             }
-        __syncthreads();
-        return;
-    }
-    if constexpr (FS == 2) __syncthreads();
-#pragma unroll
-    for (int t = 0; t < TB; ++t) {
-        const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int k = kb * 16 + (lane >> 4) * 4 + v;
-            float mm[T2];
-#pragma unroll
-            for (int lf = 0; lf < NF4; ++lf)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) mm[group_f4<M, FS, G>(lf) * 4 + q] = acc[t][4 * lf + q][v];
-            float yy[M * M];
-            output_tile_transform_rows<M, ROWS>(mm, yy);
-            if constexpr (FS == 2) {
-                const float *src = part + (((long long)(kbl * TB + t) * 4 + v) * M * M) * 64 + lane;
-#pragma unroll
-                for (int e = 0; e < M * M; ++e) yy[e] += src[e * 64];
-            }
-            if (ti.ok && k < g.K)
-                store_tile<M>(y + ((long long)ti.n * g.K + k) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
         }
     }
 }
 
+// Persistent warp-specialised fused kernel: one workgroup per compute unit
+// (register and LDS use allow one), each walking a contiguous range of items
+// (tile group, output-channel group); workgroups adjacent in that order sit on
+// the same XCD.  Producers and consumers run the items' stages as one sequence,
+// so the next item's first input tiles load and transform while the consumers
+// finish the current item's output transform and stores.
 template <int M, int TB, int FS, bool VX>
 __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__ x,
                                                        const floatx4 *__restrict__ wt,
-                                                       float *__restrict__ y, Geometry g, int vec) {
+                                                       float *__restrict__ y, Geometry g, int vec,
+                                                       int n_tgroups, int n_items) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB;
     constexpr int CC = 256 / R;
     constexpr int BUF = F4 * CC * R;
-    constexpr int KBW = 4 / FS;  // output blocks per workgroup
-    __shared__ floatx4 lds[2 * BUF];
+    constexpr int COMB = FS == 1 ? 0 : 2 * M * M * 64 / 4;  // float4s of the combine slot
+    __shared__ floatx4 lds[2 * BUF + COMB];
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int lane = tid & 63;
-    const int lin = xcd_contiguous_id(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
-    const int tgrp = lin % gridDim.x;
-    const int kgrp = lin / gridDim.x;
-    const int tile0 = tgrp * R;
+    const int wg = xcd_contiguous_id(blockIdx.x, gridDim.x);
+    const int it0 = (int)((long long)wg * n_items / gridDim.x);
+    const int it1 = (int)((long long)(wg + 1) * n_items / gridDim.x);
     const long long HW = (long long)g.H * g.W;
     const int stages = (g.C + CC - 1) / CC;
+    const int nrounds = (it1 - it0) * stages;  // stages this workgroup processes
 
     if (wave >= 4) {
         // ---------------- producer: load + input transform -> LDS ----------------
@@ -723,51 +742,61 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         // VX: row-vector loads with DPP halo exchange; otherwise one load per element
         using Loader = typename std::conditional<VX, RowTile<M>, BufTile<M, (M <= 2)>>::type;
         Loader ld;
-        if constexpr (VX) ld.init(g, decode_tile(g, tile0 + tr), cl, lane & 15);
-        else ld.init(g, decode_tile(g, tile0 + tr), cl);
+        auto init_item = [&](int it) {
+            const TileIdx ti = decode_tile(g, (it % n_tgroups) * R + tr);
+            if constexpr (VX) ld.init(g, ti, cl, lane & 15);
+            else ld.init(g, ti, cl);
+        };
         const bool maskcols = (g.W % M) != 0;
         const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
         const bool ctail = (g.C % CC) != 0;
-        auto load_stage = [&](int st, float *d) {
+        // load stage r of the sequence (item it0 + r / stages, channel stage r % stages)
+        auto load_stage = [&](int r, float *d) {
+            const int st = r % stages;
+            if (st == 0) init_item(it0 + r / stages);
             const long long cbase = (long long)st * CC * HW;
             const int32x4 rs = make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4));
             if constexpr (VX) ld.load(rs, d, maskcols);
             else ld.load(rs, d);
         };
-        // round st: prefetch stage st+1, transform stage st into buffer st&1, barrier
-        auto round = [&](int st, float *dcur, float *dnext) {
-            if (st + 1 < stages) load_stage(st + 1, dnext);
-            if (st < stages) {
+        // round r: prefetch stage r+1, transform stage r into buffer r&1, then the
+        // barriers of a consumer epilogue that runs in this round, then the stage barrier
+        auto round = [&](int r, float *dcur, float *dnext) {
+            if (r + 1 < nrounds) load_stage(r + 1, dnext);
+            if (r < nrounds) {
+                const int st = r % stages;
                 // channels past C (last stage only, when C % CC != 0) store zeros
                 const bool zero = ctail && st == stages - 1 && st * CC + cl >= g.C;
-                floatx4 *buf = lds + (st & 1) * BUF + cl * R + tr;
+                floatx4 *buf = lds + (r & 1) * BUF + cl * R + tr;
                 input_tile_transform_emit<M>(dcur, [&](int f4, float a, float b, float c, float e) {
                     buf[f4 * CC * R] = zero ? floatx4{0.f, 0.f, 0.f, 0.f} : floatx4{a, b, c, e};
                 });
             }
+            if (combine_barriers<FS>() && r >= 2 && (r - 2) % stages == stages - 1)
+                for (int b = 0; b < combine_barriers<FS>(); ++b) __syncthreads();
             __syncthreads();
         };
         float d0[T2], d1[T2];
-        load_stage(0, d0);
-        int st = 0;
-        for (; st + 1 <= stages; st += 2) {
-            round(st, d0, d1);
-            round(st + 1, d1, d0);
+        if (nrounds > 0) load_stage(0, d0);
+        int r = 0;
+        for (; r + 1 <= nrounds; r += 2) {
+            round(r, d0, d1);
+            round(r + 1, d1, d0);
         }
-        if (st <= stages) round(st, d0, d1);
-        if constexpr (FS == 2) __syncthreads();  // matches the consumers' combine barrier
+        if (r <= nrounds) round(r, d0, d1);
+        if (nrounds > 0)  // epilogue of the last item
+            for (int b = 0; b < combine_barriers<FS>(); ++b) __syncthreads();
         return;
     }
 
     // ---------------- consumers ----------------
+    float *comb = reinterpret_cast<float *>(lds + 2 * BUF);
     const int kbl = wave / FS;
-    const int kb = kgrp * KBW + kbl;
-    const floatx4 *wk = wt + (long long)kb * g.Cs * F4 * 64 + lane;
     if constexpr (FS == 1) {
-        ws_consume<M, TB, 1, 0>(lds, wk, y, g, tile0, kb, kbl, lane, stages, vec);
+        ws_consume<M, TB, 1, 0>(lds, comb, wt, y, g, it0, it1, n_tgroups, kbl, lane, stages, vec);
     } else {
-        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, wk, y, g, tile0, kb, kbl, lane, stages, vec);
-        else ws_consume<M, TB, FS, 1>(lds, wk, y, g, tile0, kb, kbl, lane, stages, vec);
+        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, wt, y, g, it0, it1, n_tgroups, kbl, lane, stages, vec);
+        else ws_consume<M, TB, FS, 1>(lds, comb, wt, y, g, it0, it1, n_tgroups, kbl, lane, stages, vec);
     }
 }
 
@@ -921,19 +950,21 @@ FusedCfg fused_cfg_default(const Geometry &g) {
 
 template <int M, int TB, int FS>
 static void launch_ws_t(const Geometry &g, const float *x, const float *wt, float *y, bool vec,
-                        hipStream_t s) {
+                        int num_cus, hipStream_t s) {
     constexpr int KBW = 4 / FS;
-    dim3 block(512);
-    dim3 grid((unsigned)((g.ntiles + 16 * TB - 1) / (16 * TB)), (unsigned)((g.Kb + KBW - 1) / KBW));
+    const int n_tgroups = (g.ntiles + 16 * TB - 1) / (16 * TB);
+    const int n_items = n_tgroups * ((g.Kb + KBW - 1) / KBW);
+    const int nwg = n_items < num_cus ? n_items : num_cus;
+    dim3 block(512), grid((unsigned)nwg);
     // row-vector input loads need every row start aligned to the vector width
     const unsigned vw = (M == 4) ? 16u : 8u;
     const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
     if (vx)
         hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, true>), grid, block, 0, s, x,
-                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0);
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_tgroups, n_items);
     else
         hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, false>), grid, block, 0, s, x,
-                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0);
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_tgroups, n_items);
 }
 
 template <int M, int TB>
@@ -963,9 +994,9 @@ hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, 
         const uintptr_t ya = reinterpret_cast<uintptr_t>(y);
         const bool vec = (g.m == 4) ? (g.W % 4 == 0 && ya % 16 == 0) : (g.W % 2 == 0 && ya % 8 == 0);
         switch (g.m) {
-            case 2: launch_ws_t<2, 2, 1>(g, x, wt, y, vec, s); break;
-            case 4: launch_ws_t<4, 1, 1>(g, x, wt, y, vec, s); break;
-            default: launch_ws_t<6, 1, 2>(g, x, wt, y, vec, s); break;
+            case 2: launch_ws_t<2, 2, 1>(g, x, wt, y, vec, cfg.num_cus, s); break;
+            case 4: launch_ws_t<4, 1, 1>(g, x, wt, y, vec, cfg.num_cus, s); break;
+            default: launch_ws_t<6, 1, 2>(g, x, wt, y, vec, cfg.num_cus, s); break;
         }
         return hipGetLastError();
     }
