@@ -513,17 +513,6 @@ __global__ void __launch_bounds__(256) fused_shared_kernel(const float *__restri
 }
 
 // ---------------------------------------------------------------------------
-// Workgroups are dispatched to the 8 XCDs round-robin by linear id.  This remaps
-// the linear id so that each XCD receives one contiguous range of logical ids:
-// neighbouring tile groups then run on the same XCD and share the halo rows of
-// their input tiles (and the transformed kernels) in that XCD's L2.
-__device__ __forceinline__ int xcd_contiguous_id(int lin, int total) {
-    constexpr int kXcds = 8;
-    const int q = total / kXcds, r = total % kXcds;
-    const int xcd = lin % kXcds, idx = lin / kXcds;
-    return xcd * q + (xcd < r ? xcd : r) + idx;
-}
-
 // Store one m x m output tile of plane yp (clipped to H x W).  vec: rows may be
 // written with m-float vector stores (16-byte aligned for m = 4, 8-byte for m = 2, 6).
 template <int M>
@@ -609,14 +598,14 @@ struct GroupF4 {
 template <int FS>
 constexpr int combine_barriers() { return FS == 1 ? 0 : 8; }
 
-// Consumer of the persistent warp-specialised kernel: items it0 .. it1-1, each
-// one (tile group, output-channel group) pair, as one continuous sequence of
-// stages shared with the producers.
+// Consumer of the persistent warp-specialised kernel: items first + i*stride,
+// i < count, each one (tile group, output-channel group) pair, as one
+// continuous sequence of stages shared with the producers.
 template <int M, int TB, int FS, int G>
 __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb,  // shared memory, written by other waves
                                            const floatx4 *__restrict__ wt, float *__restrict__ y,
-                                           const Geometry &g, int it0, int it1, int n_tgroups,
-                                           int kbl, int lane, int stages, int vec) {
+                                           const Geometry &g, int first, int stride, int count,
+                                           int n_kgroups, int kbl, int lane, int stages, int vec) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB, CC = 256 / R, SS = CC / 4, BUF = F4 * CC * R;
     constexpr int NF4 = F4 / FS;
@@ -628,9 +617,10 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb,  // 
 
     int q = 0;  // position in the stage sequence (selects the LDS buffer)
     __syncthreads();  // the first stage is in LDS
-    for (int it = it0; it < it1; ++it) {
-        const int tile0 = (it % n_tgroups) * R;
-        const int kb = (it / n_tgroups) * KBW + kbl;
+    for (int i = 0; i < count; ++i) {
+        const int it = first + i * stride;
+        const int tile0 = (it / n_kgroups) * R;
+        const int kb = (it % n_kgroups) * KBW + kbl;
         const floatx4 *wk = wt + (long long)kb * g.Cs * F4 * 64 + lane;
 
         floatx4 acc[TB][NF4 * 4];
@@ -707,16 +697,20 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb,  // 
 }
 
 // Persistent warp-specialised fused kernel: one workgroup per compute unit
-// (register and LDS use allow one), each walking a contiguous range of items
-// (tile group, output-channel group); workgroups adjacent in that order sit on
-// the same XCD.  Producers and consumers run the items' stages as one sequence,
-// so the next item's first input tiles load and transform while the consumers
-// finish the current item's output transform and stores.
+// (register and LDS use allow one).  Items (tile group, output-channel group)
+// are numbered with the output-channel group fastest; each XCD takes one
+// contiguous range of items and its workgroups take items from it round-robin,
+// so at any time the workgroups of an XCD work on neighbouring items: the groups
+// that re-read one tile group's input, and the tile groups whose input tiles
+// share halo rows and columns, find those in the XCD's L2.  Each workgroup runs
+// its items' stages as one sequence, so the next item's first input tiles load
+// and transform while the consumers finish the current item's output transform
+// and stores.
 template <int M, int TB, int FS, bool VX>
 __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__ x,
                                                        const floatx4 *__restrict__ wt,
                                                        float *__restrict__ y, Geometry g, int vec,
-                                                       int n_tgroups, int n_items) {
+                                                       int n_kgroups, int n_items) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB;
     constexpr int CC = 256 / R;
@@ -727,12 +721,21 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int lane = tid & 63;
-    const int wg = xcd_contiguous_id(blockIdx.x, gridDim.x);
-    const int it0 = (int)((long long)wg * n_items / gridDim.x);
-    const int it1 = (int)((long long)(wg + 1) * n_items / gridDim.x);
+    // workgroup b runs on XCD b % 8 as its (b / 8)-th workgroup
+    constexpr int kXcds = 8;
+    const int nwg = gridDim.x;
+    const int xcd = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
+    const int per = nwg / kXcds, extra = nwg % kXcds;
+    const int wg_on_xcd = per + (xcd < extra ? 1 : 0);
+    const int wg_before = xcd * per + (xcd < extra ? xcd : extra);
+    const int xcd_first = (int)((long long)n_items * wg_before / nwg);
+    const int xcd_end = (int)((long long)n_items * (wg_before + wg_on_xcd) / nwg);
+    const int first = xcd_first + j;
+    const int stride = wg_on_xcd;
+    const int count = first < xcd_end ? (xcd_end - first + stride - 1) / stride : 0;
     const long long HW = (long long)g.H * g.W;
     const int stages = (g.C + CC - 1) / CC;
-    const int nrounds = (it1 - it0) * stages;  // stages this workgroup processes
+    const int nrounds = count * stages;  // stages this workgroup processes
 
     if (wave >= 4) {
         // ---------------- producer: load + input transform -> LDS ----------------
@@ -743,17 +746,17 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         using Loader = typename std::conditional<VX, RowTile<M>, BufTile<M, (M <= 2)>>::type;
         Loader ld;
         auto init_item = [&](int it) {
-            const TileIdx ti = decode_tile(g, (it % n_tgroups) * R + tr);
+            const TileIdx ti = decode_tile(g, (it / n_kgroups) * R + tr);
             if constexpr (VX) ld.init(g, ti, cl, lane & 15);
             else ld.init(g, ti, cl);
         };
         const bool maskcols = (g.W % M) != 0;
         const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
         const bool ctail = (g.C % CC) != 0;
-        // load stage r of the sequence (item it0 + r / stages, channel stage r % stages)
+        // load stage r of the sequence (item first + (r / stages) * stride, channel stage r % stages)
         auto load_stage = [&](int r, float *d) {
             const int st = r % stages;
-            if (st == 0) init_item(it0 + r / stages);
+            if (st == 0) init_item(first + (r / stages) * stride);
             const long long cbase = (long long)st * CC * HW;
             const int32x4 rs = make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4));
             if constexpr (VX) ld.load(rs, d, maskcols);
@@ -793,10 +796,10 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     float *comb = reinterpret_cast<float *>(lds + 2 * BUF);
     const int kbl = wave / FS;
     if constexpr (FS == 1) {
-        ws_consume<M, TB, 1, 0>(lds, comb, wt, y, g, it0, it1, n_tgroups, kbl, lane, stages, vec);
+        ws_consume<M, TB, 1, 0>(lds, comb, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
     } else {
-        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, wt, y, g, it0, it1, n_tgroups, kbl, lane, stages, vec);
-        else ws_consume<M, TB, FS, 1>(lds, comb, wt, y, g, it0, it1, n_tgroups, kbl, lane, stages, vec);
+        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+        else ws_consume<M, TB, FS, 1>(lds, comb, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
     }
 }
 
@@ -953,7 +956,8 @@ static void launch_ws_t(const Geometry &g, const float *x, const float *wt, floa
                         int num_cus, hipStream_t s) {
     constexpr int KBW = 4 / FS;
     const int n_tgroups = (g.ntiles + 16 * TB - 1) / (16 * TB);
-    const int n_items = n_tgroups * ((g.Kb + KBW - 1) / KBW);
+    const int n_kgroups = (g.Kb + KBW - 1) / KBW;
+    const int n_items = n_tgroups * n_kgroups;
     const int nwg = n_items < num_cus ? n_items : num_cus;
     dim3 block(512), grid((unsigned)nwg);
     // row-vector input loads need every row start aligned to the vector width
@@ -961,10 +965,10 @@ static void launch_ws_t(const Geometry &g, const float *x, const float *wt, floa
     const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
     if (vx)
         hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, true>), grid, block, 0, s, x,
-                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_tgroups, n_items);
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_kgroups, n_items);
     else
         hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, false>), grid, block, 0, s, x,
-                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_tgroups, n_items);
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_kgroups, n_items);
 }
 
 template <int M, int TB>
