@@ -615,52 +615,68 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb,  // 
     constexpr GroupF4<M, FS, G> gm{};
     const long long HW = (long long)g.H * g.W;
 
+    static_assert(SS % 2 == 0, "channel steps are processed in pairs");
+    // Kernel operands alternate between two register sets over channel steps, so
+    // that loads for step cs+1 (or the next item's step 0) are in flight while
+    // step cs multiplies, without copies between the sets.
+    auto wptr = [&](int it) {
+        return wt + (long long)((it % n_kgroups) * KBW + kbl) * g.Cs * F4 * 64 + lane;
+    };
+    auto load_w = [&](floatx4 (&dst)[NF4], const floatx4 *wk, int cs) {
+#pragma unroll
+        for (int lf = 0; lf < NF4; ++lf) dst[lf] = wk[((long long)cs * F4 + gm.f4[lf]) * 64];
+    };
+    floatx4 wa[NF4], wb[NF4];
+    if (count > 0) load_w(wa, wptr(first), 0);
+
     int q = 0;  // position in the stage sequence (selects the LDS buffer)
     __syncthreads();  // the first stage is in LDS
     for (int i = 0; i < count; ++i) {
         const int it = first + i * stride;
         const int tile0 = (it / n_kgroups) * R;
         const int kb = (it % n_kgroups) * KBW + kbl;
-        const floatx4 *wk = wt + (long long)kb * g.Cs * F4 * 64 + lane;
+        const floatx4 *wk = wptr(it);
 
         floatx4 acc[TB][NF4 * 4];
 #pragma unroll
         for (int t = 0; t < TB; ++t)
 #pragma unroll
             for (int f = 0; f < NF4 * 4; ++f) acc[t][f] = floatx4{0.f, 0.f, 0.f, 0.f};
-        floatx4 aw[NF4];
-#pragma unroll
-        for (int lf = 0; lf < NF4; ++lf) aw[lf] = wk[gm.f4[lf] * 64];
 
+        // products of one channel step: operands w, transformed tiles from LDS step s
+        auto step = [&](const floatx4 (&w)[NF4], const floatx4 *cur, int s) {
+            const floatx4 *bp = cur + (4 * s + (lane >> 4)) * R + (lane & 15);
+#pragma unroll
+            for (int lf = 0; lf < NF4; ++lf) {
+#pragma unroll
+                for (int t = 0; t < TB; ++t) {
+                    const floatx4 b = bp[gm.f4[lf] * CC * R + t * 16];
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq)
+                        acc[t][4 * lf + qq] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            w[lf][qq], b[qq], acc[t][4 * lf + qq], 0, 0, 0);
+                }
+            }
+        };
+        // The operand loads are unconditional (indices clamped into range) so that
+        // the wait for a set never has to include loads issued after it.
+        const int last = g.Cs - 1;
         for (int j = 0; j < stages; ++j, ++q) {
             const floatx4 *cur = lds + (q & 1) * BUF;
 #pragma unroll
-            for (int s = 0; s < SS; ++s) {
+            for (int s = 0; s < SS; s += 2) {
                 const int cs = j * SS + s;
-                if (cs < g.Cs) {
-                    floatx4 an[NF4];
-                    const int cn = cs + 1 < g.Cs ? cs + 1 : cs;
-#pragma unroll
-                    for (int lf = 0; lf < NF4; ++lf)
-                        an[lf] = wk[((long long)cn * F4 + gm.f4[lf]) * 64];
-                    const floatx4 *bp = cur + (4 * s + (lane >> 4)) * R + (lane & 15);
-#pragma unroll
-                    for (int lf = 0; lf < NF4; ++lf) {
-#pragma unroll
-                        for (int t = 0; t < TB; ++t) {
-                            const floatx4 b = bp[gm.f4[lf] * CC * R + t * 16];
-#pragma unroll
-                            for (int qq = 0; qq < 4; ++qq)
-                                acc[t][4 * lf + qq] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                    aw[lf][qq], b[qq], acc[t][4 * lf + qq], 0, 0, 0);
-                        }
-                    }
-#pragma unroll
-                    for (int lf = 0; lf < NF4; ++lf) aw[lf] = an[lf];
-                }
+                load_w(wb, wk, cs + 1 < last ? cs + 1 : last);
+                __builtin_amdgcn_sched_barrier(0);
+                if (cs < g.Cs) step(wa, cur, s);
+                load_w(wa, wk, cs + 2 < last ? cs + 2 : last);
+                __builtin_amdgcn_sched_barrier(0);
+                if (cs + 1 < g.Cs) step(wb, cur, s + 1);
             }
             __syncthreads();
         }
+        // first operands of the next item (of this one again after the last item)
+        load_w(wa, wptr(i + 1 < count ? it + stride : it), 0);
 
         // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
 #pragma unroll
