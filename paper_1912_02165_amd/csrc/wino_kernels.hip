@@ -778,10 +778,13 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
             if constexpr (VX) ld.load(rs, d, maskcols);
             else ld.load(rs, d);
         };
-        // round r: prefetch stage r+1, transform stage r into buffer r&1, then the
-        // barriers of a consumer epilogue that runs in this round, then the stage barrier
+        // round r: prefetch stage r+PD, transform stage r into buffer r&1, then the
+        // barriers of a consumer epilogue that runs in this round, then the stage
+        // barrier.  PD = 2 (three rotating register sets) keeps two stages of
+        // input loads in flight where registers allow (m <= 4), else PD = 1.
+        constexpr int PD = (M <= 4) ? 2 : 1;
         auto round = [&](int r, float *dcur, float *dnext) {
-            if (r + 1 < nrounds) load_stage(r + 1, dnext);
+            if (r + PD < nrounds) load_stage(r + PD, dnext);
             if (r < nrounds) {
                 const int st = r % stages;
                 // channels past C (last stage only, when C % CC != 0) store zeros
@@ -795,14 +798,27 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
                 for (int b = 0; b < combine_barriers<FS>(); ++b) __syncthreads();
             __syncthreads();
         };
-        float d0[T2], d1[T2];
-        if (nrounds > 0) load_stage(0, d0);
         int r = 0;
-        for (; r + 1 <= nrounds; r += 2) {
-            round(r, d0, d1);
-            round(r + 1, d1, d0);
+        if constexpr (PD == 1) {
+            float d0[T2], d1[T2];
+            if (nrounds > 0) load_stage(0, d0);
+            for (; r + 1 <= nrounds; r += 2) {
+                round(r, d0, d1);
+                round(r + 1, d1, d0);
+            }
+            if (r <= nrounds) round(r, d0, d1);
+        } else {
+            float d0[T2], d1[T2], d2[T2];
+            if (nrounds > 0) load_stage(0, d0);
+            if (nrounds > 1) load_stage(1, d1);
+            for (; r + 2 <= nrounds; r += 3) {
+                round(r, d0, d2);
+                round(r + 1, d1, d0);
+                round(r + 2, d2, d1);
+            }
+            if (r <= nrounds) round(r, d0, d2);
+            if (r + 1 <= nrounds) round(r + 1, d1, d0);
         }
-        if (r <= nrounds) round(r, d0, d1);
         if (nrounds > 0)  // epilogue of the last item
             for (int b = 0; b < combine_barriers<FS>(); ++b) __syncthreads();
         return;
@@ -957,6 +973,7 @@ bool fused_cfg_supported(int m, const FusedCfg &cfg) {
 FusedCfg fused_cfg_default(const Geometry &g) {
     FusedCfg c;
     c.schedule = kSchedSpecialised;
+    c.num_cus = 256;  // replaced by the device's count at plan time
     c.tb = (g.m == 2) ? 2 : 1;
     c.waves = 4;
     switch (g.m) {
