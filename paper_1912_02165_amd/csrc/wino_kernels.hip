@@ -244,35 +244,52 @@ struct RowTile {
             if (t.tx * M + j < g.W) ownok |= 1u << j;
     }
 
-    __device__ __forceinline__ void load(int32x4 r, float *d, bool maskcols) const {
+    // Issues the loads of one tile without waiting for them: row a of d receives
+    // [fetched halo, own columns, -]; the halo taken from the neighbouring lanes
+    // and the masks are applied by finish(), once the data has arrived, so that
+    // loads can run several stages ahead.
+    __device__ __forceinline__ void issue(int32x4 r, float *d) const {
 #pragma unroll
         for (int a = 0; a < T; ++a) {
-            const unsigned ro = roff[a];
             // Own columns with one vector load (two 8-byte loads and one more for
-            // m = 6).  ro is below 2^31 or exactly 2^31 and own + 4*M is below
+            // m = 6).  roff is below 2^31 or exactly 2^31 and own + 4*M is below
             // 2^31, so the offsets never wrap.
-            const unsigned base = ro + own;
-            float v[M];
+            const unsigned base = roff[a] + own;
             if constexpr (M == 4) {
                 const floatx4 q = buffer_load_f32x4(r, base, 0, 0);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) v[j] = q[j];
+                for (int j = 0; j < 4; ++j) d[a * T + 1 + j] = q[j];
             } else {
 #pragma unroll
                 for (int j = 0; j < M; j += 2) {
                     const floatx2 q = buffer_load_f32x2(r, base + 4u * j, 0, 0);
-                    v[j] = q[0];
-                    v[j + 1] = q[1];
+                    d[a * T + 1 + j] = q[0];
+                    d[a * T + 2 + j] = q[1];
                 }
             }
-            const float lf = buffer_load_f32(r, fetch_l ? base - 4u : kOutside, 0, 0);
-            const float rt = buffer_load_f32(r, fetch_r ? base + 4u * M : kOutside, 0, 0);
-            const float ln = dpp_from_left(v[M - 1]);
-            const float rn = dpp_from_right(v[0]);
-            d[a * T] = first ? 0.0f : (fetch_l ? lf : ln);
+            // the one halo column a row-edge lane fetches itself (left for the first
+            // lane of a 16-lane row, right for the last): one load for both
+            d[a * T] = buffer_load_f32(r, fetch_l ? base - 4u : (fetch_r ? base + 4u * M : kOutside), 0, 0);
+        }
+    }
+
+    // The per-tile facts finish() needs, packed so they can travel with the data
+    // of a stage while the loader moves on to the next item.
+    __device__ __forceinline__ unsigned flags() const {
+        return (first ? 1u : 0u) | (last ? 2u : 0u) | (fetch_l ? 4u : 0u) | (fetch_r ? 8u : 0u) | (ownok << 8);
+    }
+
+    static __device__ __forceinline__ void finish(float *d, unsigned fl, bool maskcols) {
 #pragma unroll
-            for (int j = 0; j < M; ++j) d[a * T + 1 + j] = (maskcols && !((ownok >> j) & 1u)) ? 0.0f : v[j];
-            d[a * T + T - 1] = last ? 0.0f : (fetch_r ? rt : rn);
+        for (int a = 0; a < T; ++a) {
+            const float ln = dpp_from_left(d[a * T + M]);  // left neighbour's last own column
+            const float rn = dpp_from_right(d[a * T + 1]);  // right neighbour's first own column
+            const float h = d[a * T];                        // fetched halo, if any
+            d[a * T] = (fl & 1u) ? 0.0f : ((fl & 4u) ? h : ln);
+            d[a * T + T - 1] = (fl & 2u) ? 0.0f : ((fl & 8u) ? h : rn);
+#pragma unroll
+            for (int j = 0; j < M; ++j)
+                if (maskcols && !((fl >> (8 + j)) & 1u)) d[a * T + 1 + j] = 0.0f;
         }
     }
 };
@@ -513,6 +530,23 @@ __global__ void __launch_bounds__(256) fused_shared_kernel(const float *__restri
 }
 
 // ---------------------------------------------------------------------------
+// Store one m x m output tile that lies wholly inside the image, its first element
+// at yp (16-byte aligned for m = 4, 8-byte for m = 2, 6), rows ld floats apart.
+template <int M>
+__device__ __forceinline__ void store_rows(float *__restrict__ yp, const float *yy, int ld) {
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+        float *row = yp + (long long)i * ld;
+        if constexpr (M == 4) {
+            *reinterpret_cast<floatx4 *>(row) = floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]};
+        } else {
+#pragma unroll
+            for (int jj = 0; jj < M; jj += 2)
+                *reinterpret_cast<floatx2 *>(row + jj) = floatx2{yy[i * M + jj], yy[i * M + jj + 1]};
+        }
+    }
+}
+
 // Store one m x m output tile of plane yp (clipped to H x W).  vec: rows may be
 // written with m-float vector stores (16-byte aligned for m = 4, 8-byte for m = 2, 6).
 template <int M>
@@ -553,11 +587,9 @@ __device__ __forceinline__ void store_tile(float *__restrict__ yp, const float *
 // block w and all T^2 frequencies.  With FS = 2 (F(6), whose 64 frequencies would
 // need 256 accumulators), waves 2b and 2b+1 share output block b and each owns
 // half of the transform-domain rows; by linearity of the output transform each
-// inverse-transforms its own rows and the two partial tiles are added through
-// LDS, reusing the input-tile buffers once the channel loop is over (the result
-// matrices taking the place of dead left-hand matrices, as in Sec. 4.2).  The
-// kernel operands of the next 4-channel step are loaded while the current step
-// runs.
+// inverse-transforms its own rows and the two partial tiles are added through a
+// small LDS slot of the pair.  The kernel operands of the next 4-channel step
+// are loaded while the current step runs.
 //
 // Two waves per SIMD (a producer and a consumer) let the producers' vector work
 // overlap the matrix cores.  LDS holds two stage buffers with one barrier per
@@ -576,6 +608,12 @@ template <int M, int FS, int G>
 struct GroupF4 {
     static constexpr int N = (M + 2) * (M + 2) / 4 / FS;
     int f4[N];
+    // accumulator index (4 * position of the float4 + offset) of frequency f
+    constexpr int index(int f) const {
+        for (int i = 0; i < N; ++i)
+            if (f4[i] == f / 4) return 4 * i + f % 4;
+        return -1;
+    }
     constexpr GroupF4() : f4{} {
         constexpr unsigned rows = group_rows<M, FS, G>();
         if (FS == 1) {
@@ -591,18 +629,27 @@ struct GroupF4 {
     }
 };
 
-// Number of barriers a frequency-split (FS = 2) epilogue adds: the partial output
-// tiles of the two waves of a block pair are combined one output channel of the
-// four (v) at a time through a small LDS slot, with a barrier after the write and
-// one after the read.
-template <int FS>
-constexpr int combine_barriers() { return FS == 1 ? 0 : 8; }
+// Frequency-split (FS = 2) epilogue: the partial output tiles of the two waves of
+// a block pair are added one output channel of the four (v) at a time through an
+// LDS slot per pair.  The pair synchronises through two counters next to the
+// slot (partials written, partials read) rather than workgroup barriers, so the
+// epilogue never waits for the producer waves.  A wait gives up after kSpinLimit
+// polls, so a broken handshake ends the kernel with wrong output instead of
+// hanging it.
+constexpr unsigned kSpinLimit = 1u << 22;
+
+__device__ __forceinline__ void wait_counter(const unsigned *c, unsigned target) {
+    for (unsigned n = 0; n < kSpinLimit; ++n) {
+        if (__hip_atomic_load(c, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == target) return;
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
 
 // Consumer of the persistent warp-specialised kernel: items first + i*stride,
 // i < count, each one (tile group, output-channel group) pair, as one
 // continuous sequence of stages shared with the producers.
 template <int M, int TB, int FS, int G>
-__device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb,  // shared memory, written by other waves
+__device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsigned *pairc,  // shared memory, written by other waves
                                            const floatx4 *__restrict__ wt, float *__restrict__ y,
                                            const Geometry &g, int first, int stride, int count,
                                            int n_kgroups, int kbl, int lane, int stages, int vec) {
@@ -616,26 +663,51 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb,  // 
     const long long HW = (long long)g.H * g.W;
 
     static_assert(SS % 2 == 0, "channel steps are processed in pairs");
-    // Kernel operands alternate between two register sets over channel steps, so
-    // that loads for step cs+1 (or the next item's step 0) are in flight while
-    // step cs multiplies, without copies between the sets.
-    auto wptr = [&](int it) {
-        return wt + (long long)((it % n_kgroups) * KBW + kbl) * g.Cs * F4 * 64 + lane;
-    };
-    auto load_w = [&](floatx4 (&dst)[NF4], const floatx4 *wk, int cs) {
-#pragma unroll
-        for (int lf = 0; lf < NF4; ++lf) dst[lf] = wk[((long long)cs * F4 + gm.f4[lf]) * 64];
-    };
+    // Kernel operands alternate between two register sets over channel steps (set
+    // a for even steps, b for odd ones): the loads of step u+1 are issued before
+    // the products of step u.  Every stage runs all SS steps: channels past C hold
+    // zero input tiles in LDS (and their operand indices are clamped to the last
+    // step), so an item's step sequence has a fixed even length and the loads past
+    // its end fetch the next item's first step, which arrives during the
+    // epilogue.  The loads are unconditional, so that the wait for an operand never
+    // has to include loads issued after it.
+    // Operands are read with buffer loads: the lane's offset in a VGPR, the
+    // (uniform) offset of a step of the wave's output block in an SGPR.
+    kbl = __builtin_amdgcn_readfirstlane(kbl);
+    constexpr unsigned SB = F4 * 1024u;  // bytes of one channel step of one output block
+    const int32x4 wrs = make_rsrc(reinterpret_cast<const float *>(wt),
+                                  (unsigned)g.Kb_alloc * (unsigned)g.Cs * SB);
+    const unsigned vo = (unsigned)lane * 16u;
+    auto wbase = [&](int it) { return (unsigned)(((it % n_kgroups) * KBW + kbl) * g.Cs) * SB; };
+    auto wload = [&](unsigned soff, int lf) { return buffer_load_f32x4(wrs, vo, soff + gm.f4[lf] * 1024u, 0); };
+    const int last = g.Cs - 1, nsteps = stages * SS;
     floatx4 wa[NF4], wb[NF4];
-    if (count > 0) load_w(wa, wptr(first), 0);
+    if (count > 0) {
+#pragma unroll
+        for (int lf = 0; lf < NF4; ++lf) wa[lf] = wload(wbase(first), lf);
+    }
 
     int q = 0;  // position in the stage sequence (selects the LDS buffer)
-    __syncthreads();  // the first stage is in LDS
+    unsigned seq = 0;  // partial tiles exchanged so far by this wave pair (FS = 2)
+    if constexpr (FS == 2) {
+        if (G == 0) {
+            __hip_atomic_store(pairc + 2 * kbl, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            __hip_atomic_store(pairc + 2 * kbl + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+    }
+    __syncthreads();  // the first stage is in LDS (and the pair counters are zero)
     for (int i = 0; i < count; ++i) {
         const int it = first + i * stride;
         const int tile0 = (it / n_kgroups) * R;
         const int kb = (it % n_kgroups) * KBW + kbl;
-        const floatx4 *wk = wptr(it);
+        const unsigned bk = wbase(it), bn = wbase(i + 1 < count ? it + stride : it);
+        // operands of step u of this item's sequence (u >= nsteps: the next item's)
+        auto wsrc = [&](int u) {
+            const unsigned base = u < nsteps ? bk : bn;
+            u = u < nsteps ? u : u - nsteps;
+            u = u < last ? u : last;
+            return base + (unsigned)u * SB;
+        };
 
         floatx4 acc[TB][NF4 * 4];
 #pragma unroll
@@ -658,55 +730,79 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb,  // 
                 }
             }
         };
-        // The operand loads are unconditional (indices clamped into range) so that
-        // the wait for a set never has to include loads issued after it.
-        const int last = g.Cs - 1;
+        auto load_w = [&](floatx4 (&w)[NF4], unsigned src) {
+#pragma unroll
+            for (int lf = 0; lf < NF4; ++lf) w[lf] = wload(src, lf);
+        };
         for (int j = 0; j < stages; ++j, ++q) {
             const floatx4 *cur = lds + (q & 1) * BUF;
 #pragma unroll
             for (int s = 0; s < SS; s += 2) {
-                const int cs = j * SS + s;
-                load_w(wb, wk, cs + 1 < last ? cs + 1 : last);
+                const int u = j * SS + s;
+                load_w(wb, wsrc(u + 1));
                 __builtin_amdgcn_sched_barrier(0);
-                if (cs < g.Cs) step(wa, cur, s);
-                load_w(wa, wk, cs + 2 < last ? cs + 2 : last);
+                step(wa, cur, s);
+                load_w(wa, wsrc(u + 2));
                 __builtin_amdgcn_sched_barrier(0);
-                if (cs + 1 < g.Cs) step(wb, cur, s + 1);
+                step(wb, cur, s + 1);
             }
             __syncthreads();
         }
-        // first operands of the next item (of this one again after the last item)
-        load_w(wa, wptr(i + 1 < count ? it + stride : it), 0);
 
         // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
+        // When every tile of the wave lies wholly inside the image and all 16 output
+        // channels of the block exist (a wave-uniform test), rows are stored
+        // unclipped.
 #pragma unroll
         for (int t = 0; t < TB; ++t) {
             const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
+            const bool inside = ti.ok && ti.ty * M + M <= g.H && ti.tx * M + M <= g.W;
+            const bool whole = vec != 0 && (kb + 1) * 16 <= g.K &&
+                               __builtin_amdgcn_ballot_w64(!inside) == 0;
+            // P = Mm A, one transform-domain row i at a time for the lane's four
+            // output channels, so the accumulators of a row are dead once it is done
+            float pm[4][T][M];  // [v][i][c]; rows outside ROWS are not used
+#pragma unroll
+            for (int i = 0; i < T; ++i) {
+                if (!((ROWS >> i) & 1u)) continue;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    float row[T];
+#pragma unroll
+                    for (int jj = 0; jj < T; ++jj) row[jj] = acc[t][gm.index(i * T + jj)][v];
+                    at_1d<M, 1, 1>(row, pm[v][i]);
+                }
+            }
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int k = kb * 16 + (lane >> 4) * 4 + v;
-                float mm[T2];
-#pragma unroll
-                for (int lf = 0; lf < NF4; ++lf)
-#pragma unroll
-                    for (int qq = 0; qq < 4; ++qq) mm[gm.f4[lf] * 4 + qq] = acc[t][4 * lf + qq][v];
+                // Y = A^T P, column by column
                 float yy[M * M];
-                output_tile_transform_rows<M, ROWS>(mm, yy);
+#pragma unroll
+                for (int c = 0; c < M; ++c) at_1d_rows<M, M, M, ROWS>(&pm[v][0][c], yy + c);
                 if constexpr (FS == 2) {
                     float *slot = comb + (long long)kbl * M * M * 64 + lane;
+                    unsigned *written = pairc + 2 * kbl, *read = pairc + 2 * kbl + 1;
                     if constexpr (G == 1) {
+                        wait_counter(read, seq);  // the slot's previous partial has been read
 #pragma unroll
                         for (int e = 0; e < M * M; ++e) slot[e * 64] = yy[e];
-                    }
-                    __syncthreads();
-                    if constexpr (G == 0) {
+                        __hip_atomic_store(written, seq + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    } else {
+                        wait_counter(written, seq + 1);
 #pragma unroll
                         for (int e = 0; e < M * M; ++e) yy[e] += slot[e * 64];
+                        __hip_atomic_store(read, seq + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
                     }
-                    __syncthreads();
+                    ++seq;
                 }
-                if (G == 0 && ti.ok && k < g.K)
-                    store_tile<M>(y + ((long long)ti.n * g.K + k) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
+                if constexpr (G == 0) {
+                    if (whole)
+                        store_rows<M>(y + ((long long)ti.n * g.K + k) * HW + (long long)ti.ty * M * g.W + ti.tx * M,
+                                      yy, g.W);
+                    else if (ti.ok && k < g.K)
+                        store_tile<M>(y + ((long long)ti.n * g.K + k) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
+                }
             }
         }
     }
@@ -731,7 +827,8 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     constexpr int R = 16 * TB;
     constexpr int CC = 256 / R;
     constexpr int BUF = F4 * CC * R;
-    constexpr int COMB = FS == 1 ? 0 : 2 * M * M * 64 / 4;  // float4s of the combine slot
+    // float4s of the combine slots and the pair counters (FS = 2)
+    constexpr int COMB = FS == 1 ? 0 : 2 * M * M * 64 / 4 + 1;
     __shared__ floatx4 lds[2 * BUF + COMB];
 
     const int tid = threadIdx.x;
@@ -770,22 +867,31 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
         const bool ctail = (g.C % CC) != 0;
         // load stage r of the sequence (item first + (r / stages) * stride, channel stage r % stages)
-        auto load_stage = [&](int r, float *d) {
+        auto load_stage = [&](int r, float *d, unsigned &fl) {
             const int st = r % stages;
             if (st == 0) init_item(first + (r / stages) * stride);
             const long long cbase = (long long)st * CC * HW;
             const int32x4 rs = make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4));
-            if constexpr (VX) ld.load(rs, d, maskcols);
-            else ld.load(rs, d);
+            if constexpr (VX) {
+                ld.issue(rs, d);
+                fl = ld.flags();
+            } else {
+                ld.load(rs, d);
+            }
         };
-        // round r: prefetch stage r+PD, transform stage r into buffer r&1, then the
-        // barriers of a consumer epilogue that runs in this round, then the stage
-        // barrier.  PD = 2 (three rotating register sets) keeps two stages of
-        // input loads in flight where registers allow (m <= 4), else PD = 1.
+        // round r: issue the loads of stage r+PD, finish and transform stage r into
+        // buffer r&1, then the stage barrier.  PD = 2 (three rotating register sets)
+        // keeps two stages of input loads in flight where registers allow (m <= 4),
+        // else PD = 1.
         constexpr int PD = (M <= 4) ? 2 : 1;
-        auto round = [&](int r, float *dcur, float *dnext) {
-            if (r + PD < nrounds) load_stage(r + PD, dnext);
+        // The loads of round r + PD are issued unconditionally (past the last stage
+        // they read tiles of items beyond this workgroup's, or nothing, at offsets
+        // outside the buffer), so that the wait for a stage's data never has to
+        // cover loads issued after it.
+        auto round = [&](int r, float *dcur, unsigned fcur, float *dnext, unsigned &fnext) {
+            load_stage(r + PD, dnext, fnext);
             if (r < nrounds) {
+                if constexpr (VX) RowTile<M>::finish(dcur, fcur, maskcols);
                 const int st = r % stages;
                 // channels past C (last stage only, when C % CC != 0) store zeros
                 const bool zero = ctail && st == stages - 1 && st * CC + cl >= g.C;
@@ -794,44 +900,43 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
                     buf[f4 * CC * R] = zero ? floatx4{0.f, 0.f, 0.f, 0.f} : floatx4{a, b, c, e};
                 });
             }
-            if (combine_barriers<FS>() && r >= 2 && (r - 2) % stages == stages - 1)
-                for (int b = 0; b < combine_barriers<FS>(); ++b) __syncthreads();
             __syncthreads();
         };
         int r = 0;
         if constexpr (PD == 1) {
             float d0[T2], d1[T2];
-            if (nrounds > 0) load_stage(0, d0);
+            unsigned f0 = 0, f1 = 0;
+            load_stage(0, d0, f0);
             for (; r + 1 <= nrounds; r += 2) {
-                round(r, d0, d1);
-                round(r + 1, d1, d0);
+                round(r, d0, f0, d1, f1);
+                round(r + 1, d1, f1, d0, f0);
             }
-            if (r <= nrounds) round(r, d0, d1);
+            if (r <= nrounds) round(r, d0, f0, d1, f1);
         } else {
             float d0[T2], d1[T2], d2[T2];
-            if (nrounds > 0) load_stage(0, d0);
-            if (nrounds > 1) load_stage(1, d1);
+            unsigned f0 = 0, f1 = 0, f2 = 0;
+            load_stage(0, d0, f0);
+            load_stage(1, d1, f1);
             for (; r + 2 <= nrounds; r += 3) {
-                round(r, d0, d2);
-                round(r + 1, d1, d0);
-                round(r + 2, d2, d1);
+                round(r, d0, f0, d2, f2);
+                round(r + 1, d1, f1, d0, f0);
+                round(r + 2, d2, f2, d1, f1);
             }
-            if (r <= nrounds) round(r, d0, d2);
-            if (r + 1 <= nrounds) round(r + 1, d1, d0);
+            if (r <= nrounds) round(r, d0, f0, d2, f2);
+            if (r + 1 <= nrounds) round(r + 1, d1, f1, d0, f0);
         }
-        if (nrounds > 0)  // epilogue of the last item
-            for (int b = 0; b < combine_barriers<FS>(); ++b) __syncthreads();
         return;
     }
 
     // ---------------- consumers ----------------
     float *comb = reinterpret_cast<float *>(lds + 2 * BUF);
+    unsigned *pairc = FS == 2 ? reinterpret_cast<unsigned *>(comb + 2 * M * M * 64) : nullptr;
     const int kbl = wave / FS;
     if constexpr (FS == 1) {
-        ws_consume<M, TB, 1, 0>(lds, comb, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+        ws_consume<M, TB, 1, 0>(lds, comb, pairc, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
     } else {
-        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
-        else ws_consume<M, TB, FS, 1>(lds, comb, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, pairc, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+        else ws_consume<M, TB, FS, 1>(lds, comb, pairc, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
     }
 }
 
