@@ -21,9 +21,9 @@ struct Geometry {
 };
 
 // Fused-kernel schedule and blocking.
-enum { kSchedShared = 1, kSchedPerWave = 2, kSchedSpecialised = 3 };
+enum { kSchedShared = 1, kSchedPerWave = 2, kSchedSpecialised = 3, kSchedPersistent = 4 };
 struct FusedCfg {
-    int schedule;  // kSchedShared, kSchedPerWave or kSchedSpecialised
+    int schedule;  // kSchedShared, kSchedPerWave, kSchedSpecialised or kSchedPersistent
     int tb;        // shared: tile blocks of 16 per workgroup
     int nkb;       // per-wave: 16-channel output blocks per wave
     int waves;     // per-wave: waves per workgroup (each owns 16 tiles)

@@ -645,16 +645,39 @@ __device__ __forceinline__ void wait_counter(const unsigned *c, unsigned target)
     }
 }
 
+// Stage ring of the warp-specialised kernel: per LDS buffer (slot) a count of
+// producer waves that have filled it and of consumer waves that have drained
+// it, both only growing.  The g-th filling of a slot is complete when its fill
+// count reaches 4(g+1); the slot may be filled again once its drain count
+// reaches 4(g+1).  Waits give up after kSpinLimit polls like wait_counter.
+__device__ __forceinline__ void wait_at_least(const unsigned *c, unsigned target) {
+    for (unsigned n = 0; n < kSpinLimit; ++n) {
+        if (__hip_atomic_load(c, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= target) return;
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+// LDS stage buffers of the warp-specialised kernel: three where they fit (the
+// producers may then run up to two stages ahead), two for F(6).
+template <int M>
+constexpr int ws_slots() { return M <= 4 ? 3 : 2; }
+
+// One wave's +1 on counter c, ordered after all of the wave's LDS accesses.
+__device__ __forceinline__ void signal_wave(unsigned *c) {
+    if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
 // Consumer of the persistent warp-specialised kernel: items first + i*stride,
 // i < count, each one (tile group, output-channel group) pair, as one
 // continuous sequence of stages shared with the producers.
 template <int M, int TB, int FS, int G>
-__device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsigned *pairc,  // shared memory, written by other waves
+__device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsigned *pairc, unsigned *ring,  // shared memory, written by other waves
                                            const floatx4 *__restrict__ wt, float *__restrict__ y,
                                            const Geometry &g, int first, int stride, int count,
                                            int n_kgroups, int kbl, int lane, int stages, int vec) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB, CC = 256 / R, SS = CC / 4, BUF = F4 * CC * R;
+    constexpr int NSLOT = ws_slots<M>();
     constexpr int NF4 = F4 / FS;
     constexpr int KBW = 4 / FS;
     constexpr unsigned ROWS = group_rows<M, FS, G>();
@@ -689,13 +712,8 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
 
     int q = 0;  // position in the stage sequence (selects the LDS buffer)
     unsigned seq = 0;  // partial tiles exchanged so far by this wave pair (FS = 2)
-    if constexpr (FS == 2) {
-        if (G == 0) {
-            __hip_atomic_store(pairc + 2 * kbl, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            __hip_atomic_store(pairc + 2 * kbl + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        }
-    }
-    __syncthreads();  // the first stage is in LDS (and the pair counters are zero)
+    int slot = 0;      // LDS buffer of stage q
+    unsigned gen = 0;  // fillings of that buffer before stage q
     for (int i = 0; i < count; ++i) {
         const int it = first + i * stride;
         const int tile0 = (it / n_kgroups) * R;
@@ -735,7 +753,8 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
             for (int lf = 0; lf < NF4; ++lf) w[lf] = wload(src, lf);
         };
         for (int j = 0; j < stages; ++j, ++q) {
-            const floatx4 *cur = lds + (q & 1) * BUF;
+            wait_at_least(ring + slot, 4u * (gen + 1));  // the producers have filled it
+            const floatx4 *cur = lds + slot * BUF;
 #pragma unroll
             for (int s = 0; s < SS; s += 2) {
                 const int u = j * SS + s;
@@ -746,7 +765,11 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
                 __builtin_amdgcn_sched_barrier(0);
                 step(wb, cur, s + 1);
             }
-            __syncthreads();
+            signal_wave(ring + NSLOT + slot);  // drained
+            if (++slot == NSLOT) {
+                slot = 0;
+                ++gen;
+            }
         }
 
         // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
@@ -808,6 +831,31 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
     }
 }
 
+// Items of a persistent workgroup: first + i * stride, i < count.  Items are
+// numbered with the output-channel group fastest; each XCD takes one contiguous
+// range of them and its workgroups take items from it round-robin (workgroup b
+// runs on XCD b % 8 as its (b / 8)-th workgroup), so the workgroups of an XCD
+// work on neighbouring items at any time.
+struct ItemRange {
+    int first, stride, count;
+};
+
+__device__ __forceinline__ ItemRange item_range(int n_items) {
+    constexpr int kXcds = 8;
+    const int nwg = gridDim.x;
+    const int xcd = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
+    const int per = nwg / kXcds, extra = nwg % kXcds;
+    const int wg_on_xcd = per + (xcd < extra ? 1 : 0);
+    const int wg_before = xcd * per + (xcd < extra ? xcd : extra);
+    const int xcd_first = (int)((long long)n_items * wg_before / nwg);
+    const int xcd_end = (int)((long long)n_items * (wg_before + wg_on_xcd) / nwg);
+    ItemRange r;
+    r.first = xcd_first + j;
+    r.stride = wg_on_xcd;
+    r.count = r.first < xcd_end ? (xcd_end - r.first + r.stride - 1) / r.stride : 0;
+    return r;
+}
+
 // Persistent warp-specialised fused kernel: one workgroup per compute unit
 // (register and LDS use allow one).  Items (tile group, output-channel group)
 // are numbered with the output-channel group fastest; each XCD takes one
@@ -827,25 +875,23 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     constexpr int R = 16 * TB;
     constexpr int CC = 256 / R;
     constexpr int BUF = F4 * CC * R;
+    constexpr int NSLOT = ws_slots<M>();
     // float4s of the combine slots and the pair counters (FS = 2)
     constexpr int COMB = FS == 1 ? 0 : 2 * M * M * 64 / 4 + 1;
-    __shared__ floatx4 lds[2 * BUF + COMB];
+    constexpr int RING = (2 * NSLOT + 3) / 4;  // float4s of the ring counters
+    __shared__ floatx4 lds[NSLOT * BUF + COMB + RING];
+    float *comb = reinterpret_cast<float *>(lds + NSLOT * BUF);
+    unsigned *pairc = FS == 2 ? reinterpret_cast<unsigned *>(comb + 2 * M * M * 64) : nullptr;
+    unsigned *ring = reinterpret_cast<unsigned *>(lds + NSLOT * BUF + COMB);  // fill counts, then drain counts
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int lane = tid & 63;
-    // workgroup b runs on XCD b % 8 as its (b / 8)-th workgroup
-    constexpr int kXcds = 8;
-    const int nwg = gridDim.x;
-    const int xcd = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
-    const int per = nwg / kXcds, extra = nwg % kXcds;
-    const int wg_on_xcd = per + (xcd < extra ? 1 : 0);
-    const int wg_before = xcd * per + (xcd < extra ? xcd : extra);
-    const int xcd_first = (int)((long long)n_items * wg_before / nwg);
-    const int xcd_end = (int)((long long)n_items * (wg_before + wg_on_xcd) / nwg);
-    const int first = xcd_first + j;
-    const int stride = wg_on_xcd;
-    const int count = first < xcd_end ? (xcd_end - first + stride - 1) / stride : 0;
+    if (tid < 2 * NSLOT) ring[tid] = 0u;
+    if (FS == 2 && tid >= 64 && tid < 68) pairc[tid - 64] = 0u;
+    __syncthreads();
+    const ItemRange ir = item_range(n_items);
+    const int first = ir.first, stride = ir.stride, count = ir.count;
     const long long HW = (long long)g.H * g.W;
     const int stages = (g.C + CC - 1) / CC;
     const int nrounds = count * stages;  // stages this workgroup processes
@@ -879,10 +925,10 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
                 ld.load(rs, d);
             }
         };
-        // round r: issue the loads of stage r+PD, finish and transform stage r into
-        // buffer r&1, then the stage barrier.  PD = 2 (three rotating register sets)
-        // keeps two stages of input loads in flight where registers allow (m <= 4),
-        // else PD = 1.
+        // round r: issue the loads of stage r+PD, wait until buffer r % NSLOT is
+        // drained, finish and transform stage r into it, and count it filled.
+        // PD = 2 (three rotating register sets) keeps two stages of input loads in
+        // flight where registers allow (m <= 4), else PD = 1.
         constexpr int PD = (M <= 4) ? 2 : 1;
         // The loads of round r + PD are issued unconditionally (past the last stage
         // they read tiles of items beyond this workgroup's, or nothing, at offsets
@@ -891,16 +937,19 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         auto round = [&](int r, float *dcur, unsigned fcur, float *dnext, unsigned &fnext) {
             load_stage(r + PD, dnext, fnext);
             if (r < nrounds) {
+                const int slot = r % NSLOT;
+                const unsigned gen = (unsigned)(r / NSLOT);
                 if constexpr (VX) RowTile<M>::finish(dcur, fcur, maskcols);
+                if (gen > 0) wait_at_least(ring + NSLOT + slot, 4u * gen);
                 const int st = r % stages;
                 // channels past C (last stage only, when C % CC != 0) store zeros
                 const bool zero = ctail && st == stages - 1 && st * CC + cl >= g.C;
-                floatx4 *buf = lds + (r & 1) * BUF + cl * R + tr;
+                floatx4 *buf = lds + slot * BUF + cl * R + tr;
                 input_tile_transform_emit<M>(dcur, [&](int f4, float a, float b, float c, float e) {
                     buf[f4 * CC * R] = zero ? floatx4{0.f, 0.f, 0.f, 0.f} : floatx4{a, b, c, e};
                 });
+                signal_wave(ring + slot);
             }
-            __syncthreads();
         };
         int r = 0;
         if constexpr (PD == 1) {
@@ -929,14 +978,213 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     }
 
     // ---------------- consumers ----------------
-    float *comb = reinterpret_cast<float *>(lds + 2 * BUF);
-    unsigned *pairc = FS == 2 ? reinterpret_cast<unsigned *>(comb + 2 * M * M * 64) : nullptr;
     const int kbl = wave / FS;
     if constexpr (FS == 1) {
-        ws_consume<M, TB, 1, 0>(lds, comb, pairc, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+        ws_consume<M, TB, 1, 0>(lds, comb, pairc, ring, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
     } else {
-        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, pairc, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
-        else ws_consume<M, TB, FS, 1>(lds, comb, pairc, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, pairc, ring, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+        else ws_consume<M, TB, FS, 1>(lds, comb, pairc, ring, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Persistent fused kernel, one wave per SIMD.  On this GPU the matrix cores'
+// fp32 products and the vector ALU's fp32 arithmetic do not run concurrently on
+// one SIMD, so dedicating waves to the input transform gains no overlap; it
+// only halves the registers of the wave that holds the accumulators.  Here the
+// four waves of a workgroup each do both jobs with the full register file, which
+// allows R = 16*TB = 32 (F(4)) or 64 (F(2)) tiles per item: twice or four times
+// the reuse of every transformed-kernel operand read from L2.
+//
+// A stage is CC = 8 channels.  In stage q every wave (1) multiplies the input
+// tiles of stage q (LDS buffer q&1) by its output block's kernel operands, two
+// 4-channel steps with ping-pong operand registers as in ws_consume, (2) finishes
+// and transforms its NT tile-channels of stage q+1, whose loads were issued one
+// stage earlier, into the other buffer, (3) issues the loads of stage q+2, and
+// (4) meets the others at the one barrier of the stage.  The stages of all the
+// workgroup's items form one sequence, so the input of an item's first stage is
+// transformed during the previous item's last stage.  Items are as in
+// fused_ws_kernel; the accumulators of TB tile blocks x T^2 frequencies stay in
+// registers until the output transform.
+template <int M, int TB, bool VX>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+fused_1w_kernel(const float *__restrict__ x, const floatx4 *__restrict__ wt, float *__restrict__ y,
+                Geometry g, int vec, int n_kgroups, int n_items) {
+    constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
+    constexpr int R = 16 * TB, CC = 8, SS = CC / 4, NT = R * CC / 256;
+    constexpr int BUF = F4 * CC * R;
+    static_assert(NT >= 1 && R * CC == 256 * NT, "whole tile-channels per lane");
+    static_assert(SS == 2, "one pair of channel steps per stage");
+    __shared__ floatx4 lds[2 * BUF];
+
+    // An (empty) use of an accumulation register: the compiler then keeps the
+    // matrix-core accumulators in the accumulation registers rather than in the
+    // vector registers the transforms need.
+    asm volatile("" ::: "a0");
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const ItemRange ir = item_range(n_items);
+    const long long HW = (long long)g.H * g.W;
+    const int stages = (g.C + CC - 1) / CC;
+
+    // ---- input role: the lane's NT (tile, channel) pairs of a stage ----
+    using Loader = typename std::conditional<VX, RowTile<M>, BufTile<M, (M <= 2)>>::type;
+    Loader ld[NT];
+    int tr[NT], cl[NT];
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+        tr[n] = (tid + 256 * n) % R;
+        cl[n] = (tid + 256 * n) / R;
+    }
+    const bool maskcols = (g.W % M) != 0;
+    const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
+    const bool ctail = (g.C % CC) != 0;
+    float xd[NT][T2];
+    unsigned xf[NT];
+    // Issue the loads of stage q of the sequence (item ir.first + (q / stages) *
+    // ir.stride, channel stage q % stages).  Unconditional: past the sequence the
+    // tiles are those of later items, or outside the image (no memory access).
+    auto issue = [&](int q) {
+        const int st = q % stages;
+        if (st == 0) {
+            const int it = ir.first + (q / stages) * ir.stride;
+#pragma unroll
+            for (int n = 0; n < NT; ++n) {
+                const TileIdx ti = decode_tile(g, (it / n_kgroups) * R + tr[n]);
+                if constexpr (VX) ld[n].init(g, ti, cl[n], lane & 15);
+                else ld[n].init(g, ti, cl[n]);
+            }
+        }
+        const long long cbase = (long long)st * CC * HW;
+        const int32x4 rs = make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4));
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+            if constexpr (VX) {
+                ld[n].issue(rs, xd[n]);
+                xf[n] = ld[n].flags();
+            } else {
+                ld[n].load(rs, xd[n]);
+            }
+        }
+    };
+    // B^T d B of the lane's tiles of stage q into LDS buffer buf
+    auto transform = [&](int q, floatx4 *buf) {
+        const int st = q % stages;
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+            if constexpr (VX) RowTile<M>::finish(xd[n], xf[n], maskcols);
+            // channels past C (last stage only, when C % CC != 0) store zeros
+            const bool zero = ctail && st == stages - 1 && st * CC + cl[n] >= g.C;
+            floatx4 *b = buf + cl[n] * R + tr[n];
+            input_tile_transform_emit<M>(xd[n], [&](int f4, float a, float bb, float c, float e) {
+                b[f4 * CC * R] = zero ? floatx4{0.f, 0.f, 0.f, 0.f} : floatx4{a, bb, c, e};
+            });
+        }
+    };
+
+    // ---- matrix role: the wave's output block of the item's group ----
+    constexpr unsigned SB = F4 * 1024u;  // bytes of one channel step of one output block
+    const int32x4 wrs = make_rsrc(reinterpret_cast<const float *>(wt),
+                                  (unsigned)g.Kb_alloc * (unsigned)g.Cs * SB);
+    const unsigned vo = (unsigned)lane * 16u;
+    auto wbase = [&](int it) { return (unsigned)(((it % n_kgroups) * 4 + wave) * g.Cs) * SB; };
+    auto wload = [&](unsigned soff, int f4) { return buffer_load_f32x4(wrs, vo, soff + (unsigned)f4 * 1024u, 0); };
+    auto load_w = [&](floatx4 (&w)[F4], unsigned src) {
+#pragma unroll
+        for (int f4 = 0; f4 < F4; ++f4) w[f4] = wload(src, f4);
+    };
+    const int last = g.Cs - 1, nsteps = stages * SS;
+    floatx4 wa[F4], wb[F4];
+
+    // prologue: stage 0 into buffer 0, the loads of stage 1 in flight
+    issue(0);
+    transform(0, lds);
+    issue(1);
+    if (ir.count > 0) load_w(wa, wbase(ir.first));
+    __syncthreads();
+
+    int q = 0;  // position in the stage sequence
+    for (int i = 0; i < ir.count; ++i) {
+        const int it = ir.first + i * ir.stride;
+        const int tile0 = (it / n_kgroups) * R;
+        const int kb = (it % n_kgroups) * 4 + wave;
+        const unsigned bk = wbase(it), bn = wbase(i + 1 < ir.count ? it + ir.stride : it);
+        // operands of step u of this item's sequence (u >= nsteps: the next item's)
+        auto wsrc = [&](int u) {
+            const unsigned base = u < nsteps ? bk : bn;
+            u = u < nsteps ? u : u - nsteps;
+            u = u < last ? u : last;
+            return base + (unsigned)u * SB;
+        };
+
+        floatx4 acc[TB][T2];
+#pragma unroll
+        for (int t = 0; t < TB; ++t)
+#pragma unroll
+            for (int f = 0; f < T2; ++f) acc[t][f] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+        // products of one channel step: operands w, transformed tiles of LDS step s
+        auto step = [&](const floatx4 (&w)[F4], const floatx4 *cur, int s) {
+            const floatx4 *bp = cur + (4 * s + (lane >> 4)) * R + (lane & 15);
+#pragma unroll
+            for (int f4 = 0; f4 < F4; ++f4) {
+#pragma unroll
+                for (int t = 0; t < TB; ++t) {
+                    const floatx4 b = bp[f4 * CC * R + t * 16];
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq)
+                        acc[t][4 * f4 + qq] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            w[f4][qq], b[qq], acc[t][4 * f4 + qq], 0, 0, 0);
+                }
+            }
+        };
+        for (int j = 0; j < stages; ++j, ++q) {
+            const floatx4 *cur = lds + (q & 1) * BUF;
+            const int u = j * SS;
+            load_w(wb, wsrc(u + 1));
+            __builtin_amdgcn_sched_barrier(0);
+            step(wa, cur, 0);
+            load_w(wa, wsrc(u + 2));
+            __builtin_amdgcn_sched_barrier(0);
+            step(wb, cur, 1);
+            __builtin_amdgcn_sched_barrier(0);
+            transform(q + 1, lds + ((q + 1) & 1) * BUF);
+            issue(q + 2);
+            __syncthreads();
+        }
+
+        // Output transform Y = A^T Mm A per (output channel, tile), as in ws_consume.
+#pragma unroll
+        for (int t = 0; t < TB; ++t) {
+            const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
+            const bool inside = ti.ok && ti.ty * M + M <= g.H && ti.tx * M + M <= g.W;
+            const bool whole = vec != 0 && (kb + 1) * 16 <= g.K &&
+                               __builtin_amdgcn_ballot_w64(!inside) == 0;
+            float pm[4][T][M];  // P = Mm A, [v][i][c]
+#pragma unroll
+            for (int i2 = 0; i2 < T; ++i2) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    float row[T];
+#pragma unroll
+                    for (int jj = 0; jj < T; ++jj) row[jj] = acc[t][i2 * T + jj][v];
+                    at_1d<M, 1, 1>(row, pm[v][i2]);
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int k = kb * 16 + (lane >> 4) * 4 + v;
+                float yy[M * M];
+#pragma unroll
+                for (int c = 0; c < M; ++c) at_1d<M, M, M>(&pm[v][0][c], yy + c);
+                if (whole)
+                    store_rows<M>(y + ((long long)ti.n * g.K + k) * HW + (long long)ti.ty * M * g.W + ti.tx * M,
+                                  yy, g.W);
+                else if (ti.ok && k < g.K)
+                    store_tile<M>(y + ((long long)ti.n * g.K + k) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
+            }
+        }
     }
 }
 
@@ -1065,6 +1313,7 @@ hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt,
 bool fused_cfg_supported(int m, const FusedCfg &cfg) {
     if (m != 2 && m != 4 && m != 6) return false;
     if (cfg.schedule == kSchedSpecialised) return true;
+    if (cfg.schedule == kSchedPersistent) return m == 2;
     if (cfg.schedule == kSchedShared) return cfg.tb == 1 || (cfg.tb == 2 && m <= 4);
     if (cfg.schedule != kSchedPerWave) return false;
     if (cfg.waves < 1 || cfg.waves > 4) return false;
@@ -1110,6 +1359,24 @@ static void launch_ws_t(const Geometry &g, const float *x, const float *wt, floa
 }
 
 template <int M, int TB>
+static void launch_1w_t(const Geometry &g, const float *x, const float *wt, float *y, bool vec,
+                        int num_cus, hipStream_t s) {
+    const int n_tgroups = (g.ntiles + 16 * TB - 1) / (16 * TB);
+    const int n_kgroups = (g.Kb + 3) / 4;
+    const int n_items = n_tgroups * n_kgroups;
+    const int nwg = n_items < num_cus ? n_items : num_cus;
+    dim3 block(256), grid((unsigned)nwg);
+    const unsigned vw = (M == 4) ? 16u : 8u;
+    const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
+    if (vx)
+        hipLaunchKernelGGL((fused_1w_kernel<M, TB, true>), grid, block, 0, s, x,
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_kgroups, n_items);
+    else
+        hipLaunchKernelGGL((fused_1w_kernel<M, TB, false>), grid, block, 0, s, x,
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_kgroups, n_items);
+}
+
+template <int M, int TB>
 static void launch_shared_t(const Geometry &g, const float *x, const float *wt, float *y,
                             hipStream_t s) {
     dim3 block(256);
@@ -1132,9 +1399,13 @@ static void launch_fused_t(const Geometry &g, int waves, const float *x, const f
 hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, const float *wt,
                         float *y, hipStream_t s) {
     if (!fused_cfg_supported(g.m, cfg)) return hipErrorInvalidValue;
+    const uintptr_t ya = reinterpret_cast<uintptr_t>(y);
+    const bool vec = (g.m == 4) ? (g.W % 4 == 0 && ya % 16 == 0) : (g.W % 2 == 0 && ya % 8 == 0);
+    if (cfg.schedule == kSchedPersistent) {
+        launch_1w_t<2, 4>(g, x, wt, y, vec, cfg.num_cus, s);
+        return hipGetLastError();
+    }
     if (cfg.schedule == kSchedSpecialised) {
-        const uintptr_t ya = reinterpret_cast<uintptr_t>(y);
-        const bool vec = (g.m == 4) ? (g.W % 4 == 0 && ya % 16 == 0) : (g.W % 2 == 0 && ya % 8 == 0);
         switch (g.m) {
             case 2: launch_ws_t<2, 2, 1>(g, x, wt, y, vec, cfg.num_cus, s); break;
             case 4: launch_ws_t<4, 1, 1>(g, x, wt, y, vec, cfg.num_cus, s); break;
