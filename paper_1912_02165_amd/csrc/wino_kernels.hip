@@ -287,9 +287,14 @@ struct RowTile {
             const float h = d[a * T];                        // fetched halo, if any
             d[a * T] = (fl & 1u) ? 0.0f : ((fl & 4u) ? h : ln);
             d[a * T + T - 1] = (fl & 2u) ? 0.0f : ((fl & 8u) ? h : rn);
+        }
+        if (maskcols) {  // own columns past W (W % m != 0)
+            asm volatile("");  // keeps this a branch instead of selects run by every tile
 #pragma unroll
-            for (int j = 0; j < M; ++j)
-                if (maskcols && !((fl >> (8 + j)) & 1u)) d[a * T + 1 + j] = 0.0f;
+            for (int a = 0; a < T; ++a)
+#pragma unroll
+                for (int j = 0; j < M; ++j)
+                    if (!((fl >> (8 + j)) & 1u)) d[a * T + 1 + j] = 0.0f;
         }
     }
 };
@@ -942,11 +947,17 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
                 if constexpr (VX) RowTile<M>::finish(dcur, fcur, maskcols);
                 if (gen > 0) wait_at_least(ring + NSLOT + slot, 4u * gen);
                 const int st = r % stages;
-                // channels past C (last stage only, when C % CC != 0) store zeros
-                const bool zero = ctail && st == stages - 1 && st * CC + cl >= g.C;
+                // channels past C (last stage only, when C % CC != 0) transform zeros
+                if (ctail && st == stages - 1) {
+                    asm volatile("");  // keeps this a branch instead of selects run every stage
+                    if (st * CC + cl >= g.C) {
+#pragma unroll
+                        for (int f = 0; f < T2; ++f) dcur[f] = 0.0f;
+                    }
+                }
                 floatx4 *buf = lds + slot * BUF + cl * R + tr;
                 input_tile_transform_emit<M>(dcur, [&](int f4, float a, float b, float c, float e) {
-                    buf[f4 * CC * R] = zero ? floatx4{0.f, 0.f, 0.f, 0.f} : floatx4{a, b, c, e};
+                    buf[f4 * CC * R] = floatx4{a, b, c, e};
                 });
                 signal_wave(ring + slot);
             }
@@ -1074,11 +1085,17 @@ fused_1w_kernel(const float *__restrict__ x, const floatx4 *__restrict__ wt, flo
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
             if constexpr (VX) RowTile<M>::finish(xd[n], xf[n], maskcols);
-            // channels past C (last stage only, when C % CC != 0) store zeros
-            const bool zero = ctail && st == stages - 1 && st * CC + cl[n] >= g.C;
+            // channels past C (last stage only, when C % CC != 0) transform zeros
+            if (ctail && st == stages - 1) {
+                asm volatile("");  // keeps this a branch instead of selects run every stage
+                if (st * CC + cl[n] >= g.C) {
+#pragma unroll
+                    for (int f = 0; f < T2; ++f) xd[n][f] = 0.0f;
+                }
+            }
             floatx4 *b = buf + cl[n] * R + tr[n];
             input_tile_transform_emit<M>(xd[n], [&](int f4, float a, float bb, float c, float e) {
-                b[f4 * CC * R] = zero ? floatx4{0.f, 0.f, 0.f, 0.f} : floatx4{a, bb, c, e};
+                b[f4 * CC * R] = floatx4{a, bb, c, e};
             });
         }
     };

@@ -136,32 +136,69 @@ __device__ __forceinline__ void mac(float &acc, bool &first, float c, float v) {
     }
 }
 
+// Sum of the terms (c[a] / sc) * in[a*SI], a = A0, A0 + DA, ... < T, evaluated
+// starting with a term whose coefficient is +-1 when there is one, so that the
+// chain needs no separate multiply.
+template <int T, int SI, int A0, int DA>
+__device__ __forceinline__ float dot_unit_first(const float (&c)[T], const float *in, float sc = 1.0f) {
+    float acc = 0.f;
+    bool first = true;
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+        for (int a = A0; a < T; a += DA) {
+            const float cf = c[a] / sc;
+            const bool unit = cf == 1.0f || cf == -1.0f;
+            if ((pass == 0) == unit) mac(acc, first, cf, in[a * SI]);
+        }
+    }
+    return acc;
+}
+
+// Per row j of B^T: the magnitude shared by all nonzero odd-column entries, or 1
+// if they differ.  The odd part of a (+p, -p) row pair can then be summed with
+// +-1 coefficients and the magnitude applied once per output.
+template <int M>
+struct OddScale {
+    float s[M + 2];
+    constexpr OddScale() : s{} {
+        constexpr int T = M + 2;
+        Tables<M> tb{};
+        for (int j = 0; j < T; ++j) {
+            float m = 0.0f;
+            bool same = true;
+            for (int a = 1; a < T; a += 2) {
+                const float c = tb.bt[j][a] < 0.0f ? -tb.bt[j][a] : tb.bt[j][a];
+                if (c == 0.0f) continue;
+                if (m == 0.0f) m = c;
+                else if (m != c) same = false;
+            }
+            s[j] = (same && m != 0.0f) ? m : 1.0f;
+        }
+    }
+};
+
 // out[i*SO] = sum_a B^T[i][a] in[a*SI], i, a < T.
 template <int M, int SI, int SO>
 __device__ __forceinline__ void bt_1d(const float *in, float *out) {
     constexpr Tables<M> tb{};
+    constexpr OddScale<M> os{};
     constexpr int T = M + 2;
-    {   // p = 0 and the point at infinity: plain rows
-        float a0 = 0.f, a1 = 0.f;
-        bool f0 = true, f1 = true;
-#pragma unroll
-        for (int a = 0; a < T; ++a) {
-            mac(a0, f0, tb.bt[0][a], in[a * SI]);
-            mac(a1, f1, tb.bt[T - 1][a], in[a * SI]);
-        }
-        out[0] = a0;
-        out[(T - 1) * SO] = a1;
-    }
+    // p = 0 and the point at infinity: plain rows
+    out[0] = dot_unit_first<T, SI, 0, 1>(tb.bt[0], in);
+    out[(T - 1) * SO] = dot_unit_first<T, SI, 0, 1>(tb.bt[T - 1], in);
 #pragma unroll
     for (int j = 1; j + 1 < T - 1; j += 2) {  // (+p, -p) rows: even part +- odd part
-        float e = 0.f, o = 0.f;
-        bool fe = true, fo = true;
-#pragma unroll
-        for (int a = 0; a < T; a += 2) mac(e, fe, tb.bt[j][a], in[a * SI]);
-#pragma unroll
-        for (int a = 1; a < T; a += 2) mac(o, fo, tb.bt[j][a], in[a * SI]);
-        out[j * SO] = e + o;
-        out[(j + 1) * SO] = e - o;
+        const float e = dot_unit_first<T, SI, 0, 2>(tb.bt[j], in);
+        const float s = os.s[j];
+        const float o = dot_unit_first<T, SI, 1, 2>(tb.bt[j], in, s);
+        if (s == 1.0f) {
+            out[j * SO] = e + o;
+            out[(j + 1) * SO] = e - o;
+        } else {
+            out[j * SO] = __builtin_fmaf(s, o, e);
+            out[(j + 1) * SO] = __builtin_fmaf(-s, o, e);
+        }
     }
 }
 
