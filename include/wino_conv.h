@@ -67,9 +67,15 @@ enum {
 /* Fused-kernel schedules (wino_tuning.schedule). */
 enum {
     WINO_SCHED_AUTO = 0,
-    WINO_SCHED_SHARED = 1,   /* a workgroup transforms each input tile once into LDS and
-                                shares it across 64 output channels (default) */
-    WINO_SCHED_PER_WAVE = 2  /* every wave transforms its own input tiles in registers */
+    WINO_SCHED_SHARED = 1,      /* a workgroup transforms each input tile once into LDS and
+                                   shares it across 64 output channels */
+    WINO_SCHED_PER_WAVE = 2,    /* every wave transforms its own input tiles in registers */
+    WINO_SCHED_SPECIALISED = 3, /* default: persistent workgroups (one per compute unit) whose
+                                   producer waves load and transform input tiles into an LDS
+                                   stage ring while consumer waves run the products and the
+                                   output transform; the last round of work items is split
+                                   across workgroups when few rounds would leave units idle */
+    WINO_SCHED_PERSISTENT = 4   /* F(2x2,3x3) only: persistent, one wave per SIMD doing both */
 };
 
 /* Optional blocking overrides for the fused algorithm; a field of 0 keeps the
@@ -88,8 +94,10 @@ typedef struct {
 
 /* Create a plan for an F(m x m, 3 x 3) convolution of an N x C x H x W input
  * with K output channels, on the current HIP device, with the fused algorithm
- * and automatic blocking.  Allocates the plan's device workspace (the
- * transformed kernels, T^2 * C * K floats rounded up to the blocking).
+ * and automatic blocking.  Allocates the plan's device workspace: the
+ * transformed kernels (T^2 * C * K floats rounded up to the blocking) and, when
+ * the last round of work items is split across compute units, their partial
+ * outputs and arrival counters (zeroed here; every call leaves them zero).
  * Returns NULL (see wino_last_error) if a size is < 1, m is not 2, 4 or 6, a
  * size overflows the 32-bit offsets the kernels use (each of x and y must be
  * below 2^31 bytes), or the allocation fails. */

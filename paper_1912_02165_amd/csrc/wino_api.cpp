@@ -24,6 +24,8 @@ struct wino_plan {
     float *U;         // three-stage: transformed input  [T2][Cp][tiles_p]
     float *Mf;        // three-stage: per-frequency sums [T2][Kp][tiles_p]
     size_t U_bytes, M_bytes;
+    wino::SplitBuffers split;  // fused: partial outputs of split items and their counters
+    size_t part_bytes, cnt_bytes;
     mutable bool weights_set; // wt holds transformed kernels (set_weights or the last run)
 };
 
@@ -157,7 +159,7 @@ size_t w_bytes(const Geometry &g) { return (size_t)g.K * g.C * 9 * 4; }
 int run_body(const wino_plan *p, const float *x, float *y, hipStream_t s) {
     hipError_t e;
     if (p->algo == WINO_ALGO_FUSED) {
-        e = wino::launch_fused(p->g, p->fcfg, x, p->wt, y, s);
+        e = wino::launch_fused(p->g, p->fcfg, x, p->wt, y, p->split, s);
         if (e != hipSuccess) return hip_fail("fused kernel launch", e);
     } else {
         e = wino::launch_input_transform(p->g, x, p->U, s);
@@ -232,11 +234,6 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         hip_fail("hipGetDevice", e);
         return nullptr;
     }
-    wino_plan *p = new (std::nothrow) wino_plan();
-    if (!p) {
-        set_err("host allocation failed");
-        return nullptr;
-    }
     {
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -246,6 +243,20 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         }
         cfg.num_cus = cus;
     }
+    size_t part_bytes = 0, cnt_bytes = 0;
+    if (algo == WINO_ALGO_FUSED) {
+        const wino::SplitInfo si = wino::fused_split_info(g, cfg);
+        if (si.n_tail > 0) {
+            part_bytes = (size_t)si.n_tail * si.maxc * si.part_floats * sizeof(float);
+            cnt_bytes = (size_t)si.n_tail * sizeof(unsigned);
+        }
+    }
+    const size_t total_bytes = wt_bytes + U_bytes + M_bytes + part_bytes + cnt_bytes;
+    wino_plan *p = new (std::nothrow) wino_plan();
+    if (!p) {
+        set_err("host allocation failed");
+        return nullptr;
+    }
     p->g = g;
     p->algo = algo;
     p->fcfg = cfg;
@@ -253,6 +264,8 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
     p->wt_bytes = wt_bytes;
     p->U_bytes = U_bytes;
     p->M_bytes = M_bytes;
+    p->part_bytes = part_bytes;
+    p->cnt_bytes = cnt_bytes;
     void *ptr = nullptr;
     if ((e = hipMalloc(&ptr, wt_bytes)) != hipSuccess) goto oom;
     p->wt = static_cast<float *>(ptr);
@@ -262,17 +275,27 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         if ((e = hipMalloc(&ptr, M_bytes)) != hipSuccess) goto oom;
         p->Mf = static_cast<float *>(ptr);
     }
+    if (part_bytes) {
+        if ((e = hipMalloc(&ptr, part_bytes)) != hipSuccess) goto oom;
+        p->split.part = static_cast<float *>(ptr);
+        if ((e = hipMalloc(&ptr, cnt_bytes)) != hipSuccess) goto oom;
+        p->split.cnt = static_cast<unsigned *>(ptr);
+        // arrival counters start at zero; each split item's last contributor
+        // resets its counter, so they are zero again after every call
+        if ((e = hipMemset(p->split.cnt, 0, cnt_bytes)) != hipSuccess) goto oom;
+        if ((e = hipDeviceSynchronize()) != hipSuccess) goto oom;
+    }
     if (log_enabled())
         fprintf(stderr,
                 "[wino] plan N=%d C=%d K=%d H=%d W=%d m=%d algo=%s tiles=%d schedule=%d tb=%d "
                 "nkb=%d waves=%d workspace=%zu B\n",
                 N, C, K, H, W, m, algo == WINO_ALGO_FUSED ? "fused" : "three_stage", g.ntiles,
-                cfg.schedule, cfg.tb, cfg.nkb, cfg.waves, wt_bytes + U_bytes + M_bytes);
+                cfg.schedule, cfg.tb, cfg.nkb, cfg.waves, total_bytes);
     return p;
 oom:
     (void)hipGetLastError();
     set_err("device allocation failed (%s); workspace needs %zu bytes", hipGetErrorString(e),
-            wt_bytes + U_bytes + M_bytes);
+            total_bytes);
     wino_conv_destroy(p);
     return nullptr;
 }
@@ -286,11 +309,13 @@ void wino_conv_destroy(wino_plan *p) {
     if (p->wt) (void)hipFree(p->wt);
     if (p->U) (void)hipFree(p->U);
     if (p->Mf) (void)hipFree(p->Mf);
+    if (p->split.part) (void)hipFree(p->split.part);
+    if (p->split.cnt) (void)hipFree(p->split.cnt);
     delete p;
 }
 
 size_t wino_conv_workspace_bytes(const wino_plan *p) {
-    return p ? p->wt_bytes + p->U_bytes + p->M_bytes : 0;
+    return p ? p->wt_bytes + p->U_bytes + p->M_bytes + p->part_bytes + p->cnt_bytes : 0;
 }
 
 int wino_conv_info(const wino_plan *p, long long *n_tiles, double *direct_flops,

@@ -30,12 +30,31 @@ struct FusedCfg {
     int num_cus;   // compute units of the device (persistent grid size)
 };
 
+// Split plan of the warp-specialised fused kernel: the last round of items is
+// divided stage-wise among all workgroups; each split item's partial outputs
+// go to a plan-owned buffer and are added by the contributor that finishes last.
+struct SplitInfo {
+    int grid;              // workgroups launched
+    int n_items, n_kgroups, stages;
+    int nfull;             // full rounds of whole items (n_items / grid)
+    int tail_first, n_tail;  // items [0, tail_first) are whole, the n_tail after are split
+    unsigned tail_units;   // n_tail * stages
+    unsigned piece;        // stages per piece of a split item
+    int maxc;              // contributors (pieces) per split item
+    int part_floats;       // floats of one contributor's partial output
+};
+struct SplitBuffers {
+    float *part;           // n_tail * maxc * part_floats floats
+    unsigned *cnt;         // n_tail arrival counters, zero between calls
+};
+SplitInfo fused_split_info(const Geometry &g, const FusedCfg &cfg);
+
 // Kernel transform: w (K x C x 3 x 3) -> wt in matrix-core operand order.
 hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt, hipStream_t s);
 
 // Fused: x -> y with the transformed kernels wt.
 hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, const float *wt,
-                        float *y, hipStream_t s);
+                        float *y, const SplitBuffers &sb, hipStream_t s);
 
 // Three-stage: x -> U -> M -> y.
 hipError_t launch_input_transform(const Geometry &g, const float *x, float *U, hipStream_t s);

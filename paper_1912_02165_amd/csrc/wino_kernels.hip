@@ -134,6 +134,11 @@ __device__ floatx2 buffer_load_f32x2(int32x4 rsrc, unsigned voffset, unsigned so
     __asm("llvm.amdgcn.raw.buffer.load.v2f32");
 __device__ floatx4 buffer_load_f32x4(int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
     __asm("llvm.amdgcn.raw.buffer.load.v4f32");
+__device__ void buffer_store_f32x4(floatx4 v, int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.store.v4f32");
+// Cache-policy bit of a buffer access that makes it coherent across the device
+// (the coherence that device-scope atomic loads and stores use).
+constexpr int kDeviceCoherent = 1 << 4;
 
 __device__ __forceinline__ int32x4 make_rsrc(const float *base, unsigned bytes) {
     const unsigned long long p = reinterpret_cast<unsigned long long>(base);
@@ -142,6 +147,16 @@ __device__ __forceinline__ int32x4 make_rsrc(const float *base, unsigned bytes) 
     r[1] = (int)(unsigned)((p >> 32) & 0xffffull);  // stride 0: raw buffer
     r[2] = (int)bytes;                                 // range-checked size
     r[3] = 0x00020000;                                 // 32-bit data format
+    return r;
+}
+
+// The same resource held in scalar registers, for a base address the compiler
+// cannot prove uniform (a per-lane resource would turn every access into a loop
+// over distinct lane values).
+__device__ __forceinline__ int32x4 make_rsrc_uniform(const float *base, unsigned bytes) {
+    int32x4 r = make_rsrc(base, bytes);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = __builtin_amdgcn_readfirstlane(r[i]);
     return r;
 }
 
@@ -672,19 +687,133 @@ __device__ __forceinline__ void signal_wave(unsigned *c) {
     if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// Consumer of the persistent warp-specialised kernel: items first + i*stride,
-// i < count, each one (tile group, output-channel group) pair, as one
-// continuous sequence of stages shared with the producers.
+// Items of a persistent workgroup: first + i * stride, i < count.  Items are
+// numbered with the output-channel group fastest; each XCD takes one contiguous
+// range of them and its workgroups take items from it round-robin (workgroup b
+// runs on XCD b % 8 as its (b / 8)-th workgroup), so the workgroups of an XCD
+// work on neighbouring items at any time.
+struct ItemRange {
+    int first, stride, count;
+};
+
+__device__ __forceinline__ ItemRange item_range(int n_items) {
+    constexpr int kXcds = 8;
+    const int nwg = gridDim.x;
+    const int xcd = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
+    const int per = nwg / kXcds, extra = nwg % kXcds;
+    const int wg_on_xcd = per + (xcd < extra ? 1 : 0);
+    const int wg_before = xcd * per + (xcd < extra ? xcd : extra);
+    const int xcd_first = (int)((long long)n_items * wg_before / nwg);
+    const int xcd_end = (int)((long long)n_items * (wg_before + wg_on_xcd) / nwg);
+    ItemRange r;
+    r.first = xcd_first + j;
+    r.stride = wg_on_xcd;
+    r.count = r.first < xcd_end ? (xcd_end - r.first + r.stride - 1) / r.stride : 0;
+    return r;
+}
+
+// Work of one persistent workgroup of the warp-specialised kernel, as one
+// sequence of (item, channel stage) pairs shared by its producers and consumers:
+// first its whole items (taken as by item_range from the first n_whole items),
+// then at most one piece of a split item: each remaining item is cut into P
+// pieces of equal stage ranges ("split units" [b*L, (b+1)*L) of the remaining
+// items' stages for workgroup b, L = stages / P), which spreads a last round that
+// would otherwise leave compute units idle.  A workgroup's sequence falls into
+// segments, one per item it works on; a piece of a split item yields a partial
+// output, and the partial outputs of an item are added by whichever of its P
+// contributors finishes last.
+struct WsSplit {
+    int n_whole;          // items distributed whole (item_range over the first n_whole)
+    int tail_first;       // first split item
+    unsigned tail_units;  // split items x stages per item
+    unsigned piece;       // stages per piece of a split item (L)
+    float *part;          // partial outputs, [split item][contributor][part_floats]
+    unsigned *cnt;        // contributors arrived, per split item (zero between calls)
+    int maxc;             // contributor slots per split item
+    int part_floats;      // floats of one partial output
+};
+
+struct WsSeq {
+    int first, stride, nfull;  // whole items first + i * stride, i < nfull
+    unsigned u0, u1;           // split units [u0, u1)
+    int S;                     // stages per item
+    int tail_first, n_items;
+
+    __device__ __forceinline__ void init(const WsSplit &sp, int n_items_, int stages) {
+        S = stages;
+        n_items = n_items_;
+        const ItemRange ir = item_range(sp.n_whole);
+        first = ir.first;
+        stride = ir.stride;
+        nfull = ir.count;
+        tail_first = sp.tail_first;
+        const unsigned long long a = (unsigned long long)blockIdx.x * sp.piece;
+        u0 = (unsigned)(a < sp.tail_units ? a : sp.tail_units);
+        u1 = (unsigned)(a + sp.piece < sp.tail_units ? a + sp.piece : sp.tail_units);
+    }
+    __device__ __forceinline__ int length() const { return nfull * S + (int)(u1 - u0); }
+    __device__ __forceinline__ int segments() const {
+        return nfull + (u1 > u0 ? (int)((u1 - 1) / (unsigned)S - u0 / (unsigned)S + 1) : 0);
+    }
+    // A walker over the sequence, one stage at a time (no divisions per stage).
+    struct Cursor {
+        int k, item, st, se;
+    };
+    __device__ __forceinline__ Cursor start() const {
+        Cursor c{0, n_items, 0, 1};
+        if (segments() > 0) {
+            int sb;
+            segment(0, c.item, sb, c.se);
+            c.st = sb;
+        }
+        return c;
+    }
+    // next stage; past the end, an item that does not exist
+    __device__ __forceinline__ void advance(Cursor &c) const {
+        if (++c.st < c.se) return;
+        if (++c.k < segments()) {
+            int sb;
+            segment(c.k, c.item, sb, c.se);
+            c.st = sb;
+        } else {
+            c.item = n_items;
+            c.st = 0;
+            c.se = 1;
+        }
+    }
+    // segment k: item and its stages [sb, se); k past the end repeats the last one
+    __device__ __forceinline__ void segment(int k, int &item, int &sb, int &se) const {
+        const int ns = segments();
+        k = k < ns ? k : ns - 1;
+        if (k < nfull) {
+            item = first + k * stride;
+            sb = 0;
+            se = S;
+        } else {
+            const unsigned t = u0 / (unsigned)S + (unsigned)(k - nfull);
+            const unsigned lo = t * (unsigned)S > u0 ? t * (unsigned)S : u0;
+            const unsigned hi = (t + 1) * (unsigned)S < u1 ? (t + 1) * (unsigned)S : u1;
+            item = tail_first + (int)t;
+            sb = (int)(lo - t * (unsigned)S);
+            se = (int)(hi - t * (unsigned)S);
+        }
+    }
+};
+
+// Consumer of the persistent warp-specialised kernel: the workgroup's segments,
+// as one continuous sequence of stages shared with the producers.
 template <int M, int TB, int FS, int G>
 __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsigned *pairc, unsigned *ring,  // shared memory, written by other waves
+                                           unsigned *skc,
                                            const floatx4 *__restrict__ wt, float *__restrict__ y,
-                                           const Geometry &g, int first, int stride, int count,
-                                           int n_kgroups, int kbl, int lane, int stages, int vec) {
+                                           const Geometry &g, const WsSeq &sq, const WsSplit &sp,
+                                           int n_kgroups, int kbl, int lane, int vec) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB, CC = 256 / R, SS = CC / 4, BUF = F4 * CC * R;
     constexpr int NSLOT = ws_slots<M>();
     constexpr int NF4 = F4 / FS;
     constexpr int KBW = 4 / FS;
+    constexpr int MM = M * M;
     constexpr unsigned ROWS = group_rows<M, FS, G>();
     static_assert(FS == 1 || T == 8, "frequency split is built for F(6) only");
     constexpr GroupF4<M, FS, G> gm{};
@@ -695,8 +824,8 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
     // a for even steps, b for odd ones): the loads of step u+1 are issued before
     // the products of step u.  Every stage runs all SS steps: channels past C hold
     // zero input tiles in LDS (and their operand indices are clamped to the last
-    // step), so an item's step sequence has a fixed even length and the loads past
-    // its end fetch the next item's first step, which arrives during the
+    // step), so a segment's step sequence has an even length and the loads past
+    // its end fetch the next segment's first steps, which arrive during the
     // epilogue.  The loads are unconditional, so that the wait for an operand never
     // has to include loads issued after it.
     // Operands are read with buffer loads: the lane's offset in a VGPR, the
@@ -706,30 +835,41 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
     const int32x4 wrs = make_rsrc(reinterpret_cast<const float *>(wt),
                                   (unsigned)g.Kb_alloc * (unsigned)g.Cs * SB);
     const unsigned vo = (unsigned)lane * 16u;
+    // partial outputs of a contributor: [kbl][t][v][lane][element] floats, so a
+    // lane's output tile is contiguous (16-byte accesses)
+    static_assert(MM % 4 == 0, "output tiles are whole float4s");
+    const unsigned vlane = (unsigned)lane * MM * 4u;
+    auto poff = [&](int t, int v) { return (unsigned)((((kbl * TB + t) * 4 + v) * 64) * MM) * 4u; };
     auto wbase = [&](int it) { return (unsigned)(((it % n_kgroups) * KBW + kbl) * g.Cs) * SB; };
     auto wload = [&](unsigned soff, int lf) { return buffer_load_f32x4(wrs, vo, soff + gm.f4[lf] * 1024u, 0); };
-    const int last = g.Cs - 1, nsteps = stages * SS;
+    const int last = g.Cs - 1;
+    const int nseg = sq.segments();
     floatx4 wa[NF4], wb[NF4];
-    if (count > 0) {
+    int item = 0, sb = 0, se = 0;
+    if (nseg > 0) {
+        sq.segment(0, item, sb, se);
+        const unsigned c0 = (unsigned)(sb * SS < last ? sb * SS : last);
 #pragma unroll
-        for (int lf = 0; lf < NF4; ++lf) wa[lf] = wload(wbase(first), lf);
+        for (int lf = 0; lf < NF4; ++lf) wa[lf] = wload(wbase(item) + c0 * SB, lf);
     }
 
     int q = 0;  // position in the stage sequence (selects the LDS buffer)
     unsigned seq = 0;  // partial tiles exchanged so far by this wave pair (FS = 2)
+    unsigned nsk = 0;  // partial-output epilogues so far
     int slot = 0;      // LDS buffer of stage q
     unsigned gen = 0;  // fillings of that buffer before stage q
-    for (int i = 0; i < count; ++i) {
-        const int it = first + i * stride;
-        const int tile0 = (it / n_kgroups) * R;
-        const int kb = (it % n_kgroups) * KBW + kbl;
-        const unsigned bk = wbase(it), bn = wbase(i + 1 < count ? it + stride : it);
-        // operands of step u of this item's sequence (u >= nsteps: the next item's)
+    for (int k = 0; k < nseg; ++k) {
+        if (k > 0) sq.segment(k, item, sb, se);
+        int item2, sb2, se2;
+        sq.segment(k + 1, item2, sb2, se2);
+        const int nsteps = (se - sb) * SS;
+        const unsigned bk = wbase(item), bn = wbase(item2);
+        // operands of step u of this segment (u >= nsteps: the next segment's)
         auto wsrc = [&](int u) {
-            const unsigned base = u < nsteps ? bk : bn;
-            u = u < nsteps ? u : u - nsteps;
-            u = u < last ? u : last;
-            return base + (unsigned)u * SB;
+            const bool cur = u < nsteps;
+            int c = cur ? sb * SS + u : sb2 * SS + (u - nsteps);
+            c = c < last ? c : last;
+            return (cur ? bk : bn) + (unsigned)c * SB;
         };
 
         floatx4 acc[TB][NF4 * 4];
@@ -757,7 +897,7 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
 #pragma unroll
             for (int lf = 0; lf < NF4; ++lf) w[lf] = wload(src, lf);
         };
-        for (int j = 0; j < stages; ++j, ++q) {
+        for (int j = 0; j < se - sb; ++j, ++q) {
             wait_at_least(ring + slot, 4u * (gen + 1));  // the producers have filled it
             const floatx4 *cur = lds + slot * BUF;
 #pragma unroll
@@ -777,105 +917,175 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
             }
         }
 
-        // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W.
-        // When every tile of the wave lies wholly inside the image and all 16 output
-        // channels of the block exist (a wave-uniform test), rows are stored
-        // unclipped.
+        // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W,
+        // into yy; emit(t, v, k, ti, yy) consumes each finished output tile.
+        const int tile0 = (item / n_kgroups) * R;
+        const int kb = (item % n_kgroups) * KBW + kbl;
+        auto out_tiles = [&](auto emit) {
 #pragma unroll
-        for (int t = 0; t < TB; ++t) {
-            const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
-            const bool inside = ti.ok && ti.ty * M + M <= g.H && ti.tx * M + M <= g.W;
-            const bool whole = vec != 0 && (kb + 1) * 16 <= g.K &&
-                               __builtin_amdgcn_ballot_w64(!inside) == 0;
-            // P = Mm A, one transform-domain row i at a time for the lane's four
-            // output channels, so the accumulators of a row are dead once it is done
-            float pm[4][T][M];  // [v][i][c]; rows outside ROWS are not used
+            for (int t = 0; t < TB; ++t) {
+                const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
+                // P = Mm A, one transform-domain row i at a time for the lane's four
+                // output channels, so the accumulators of a row are dead once it is done
+                float pm[4][T][M];  // [v][i][c]; rows outside ROWS are not used
 #pragma unroll
-            for (int i = 0; i < T; ++i) {
-                if (!((ROWS >> i) & 1u)) continue;
+                for (int i = 0; i < T; ++i) {
+                    if (!((ROWS >> i) & 1u)) continue;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        float row[T];
+#pragma unroll
+                        for (int jj = 0; jj < T; ++jj) row[jj] = acc[t][gm.index(i * T + jj)][v];
+                        at_1d<M, 1, 1>(row, pm[v][i]);
+                    }
+                }
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    float row[T];
+                    // Y = A^T P, column by column
+                    float yy[MM];
 #pragma unroll
-                    for (int jj = 0; jj < T; ++jj) row[jj] = acc[t][gm.index(i * T + jj)][v];
-                    at_1d<M, 1, 1>(row, pm[v][i]);
-                }
-            }
+                    for (int c = 0; c < M; ++c) at_1d_rows<M, M, M, ROWS>(&pm[v][0][c], yy + c);
+                    if constexpr (FS == 2) {
+                        float *cslot = comb + (long long)kbl * MM * 64 + lane;
+                        unsigned *written = pairc + 2 * kbl, *read = pairc + 2 * kbl + 1;
+                        if constexpr (G == 1) {
+                            wait_counter(read, seq);  // the slot's previous partial has been read
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int k = kb * 16 + (lane >> 4) * 4 + v;
-                // Y = A^T P, column by column
-                float yy[M * M];
+                            for (int e = 0; e < MM; ++e) cslot[e * 64] = yy[e];
+                            __hip_atomic_store(written, seq + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+                        } else {
+                            wait_counter(written, seq + 1);
 #pragma unroll
-                for (int c = 0; c < M; ++c) at_1d_rows<M, M, M, ROWS>(&pm[v][0][c], yy + c);
-                if constexpr (FS == 2) {
-                    float *slot = comb + (long long)kbl * M * M * 64 + lane;
-                    unsigned *written = pairc + 2 * kbl, *read = pairc + 2 * kbl + 1;
-                    if constexpr (G == 1) {
-                        wait_counter(read, seq);  // the slot's previous partial has been read
-#pragma unroll
-                        for (int e = 0; e < M * M; ++e) slot[e * 64] = yy[e];
-                        __hip_atomic_store(written, seq + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-                    } else {
-                        wait_counter(written, seq + 1);
-#pragma unroll
-                        for (int e = 0; e < M * M; ++e) yy[e] += slot[e * 64];
-                        __hip_atomic_store(read, seq + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+                            for (int e = 0; e < MM; ++e) yy[e] += cslot[e * 64];
+                            __hip_atomic_store(read, seq + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+                        }
+                        ++seq;
                     }
-                    ++seq;
-                }
-                if constexpr (G == 0) {
-                    if (whole)
-                        store_rows<M>(y + ((long long)ti.n * g.K + k) * HW + (long long)ti.ty * M * g.W + ti.tx * M,
-                                      yy, g.W);
-                    else if (ti.ok && k < g.K)
-                        store_tile<M>(y + ((long long)ti.n * g.K + k) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
+                    if constexpr (G == 0) emit(t, v, kb * 16 + (lane >> 4) * 4 + v, ti, yy);
                 }
             }
+        };
+        auto store = [&](const TileIdx &ti, int k_out, const float *yy, bool whole) {
+            if (whole)
+                store_rows<M>(y + ((long long)ti.n * g.K + k_out) * HW + (long long)ti.ty * M * g.W + ti.tx * M,
+                              yy, g.W);
+            else if (ti.ok && k_out < g.K)
+                store_tile<M>(y + ((long long)ti.n * g.K + k_out) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
+        };
+        // When every tile of the wave lies wholly inside the image and all 16 output
+        // channels of the block exist (a wave-uniform test), rows are stored unclipped.
+        auto whole_of = [&](const TileIdx &ti) {
+            const bool inside = ti.ok && ti.ty * M + M <= g.H && ti.tx * M + M <= g.W;
+            return vec != 0 && (kb + 1) * 16 <= g.K && __builtin_amdgcn_ballot_w64(!inside) == 0;
+        };
+        // the last contributor of a split item: y = sum of the partials in order
+        auto sum_partials = [&](const float *pbase_, int ncontrib_) {
+            const int32x4 all = make_rsrc_uniform(pbase_, (unsigned)(ncontrib_ * sp.part_floats) * 4u);
+            for (int t = 0; t < TB; ++t) {
+                const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
+                const bool whole = whole_of(ti);
+                for (int v = 0; v < 4; ++v) {
+                    float yy[MM];
+#pragma unroll
+                    for (int e = 0; e < MM; ++e) yy[e] = 0.0f;
+                    // CH contributors' partials are loaded before any is added (one
+                    // memory round trip per CH contributors); the additions keep
+                    // contributor order
+                    constexpr int CH = MM >= 36 ? 2 : 4;
+                    for (int jc0 = 0; jc0 < ncontrib_; jc0 += CH) {
+                        floatx4 pv[CH][MM / 4];
+#pragma unroll
+                        for (int c = 0; c < CH; ++c) {
+                            const int jc = jc0 + c < ncontrib_ ? jc0 + c : ncontrib_ - 1;
+                            const unsigned o = (unsigned)(jc * sp.part_floats) * 4u + poff(t, v);
+#pragma unroll
+                            for (int e = 0; e < MM / 4; ++e) pv[c][e] = buffer_load_f32x4(all, vlane, o + e * 16u, kDeviceCoherent);
+                        }
+#pragma unroll
+                        for (int c = 0; c < CH; ++c) {
+                            if (jc0 + c < ncontrib_) {
+#pragma unroll
+                                for (int e = 0; e < MM; ++e) yy[e] += pv[c][e / 4][e % 4];
+                            }
+                        }
+                    }
+                    store(ti, kb * 16 + (lane >> 4) * 4 + v, yy, whole);
+                }
+            }
+        };
+        // A segment that covers only part of its item's stages yields a partial
+        // output (Sec. 3: the output transform is linear, so partial sums over
+        // channels can be inverse-transformed separately and added).  Each
+        // contributor writes its partial; the one that arrives last adds all
+        // partials in contributor order (a fixed order, so the result is
+        // reproducible) and stores y.  Partials are written and read with
+        // device-coherent accesses; a writer's stores have completed before its
+        // arrival is counted.
+        const bool partial = !(sb == 0 && se == sq.S);
+        const unsigned t_split = (unsigned)__builtin_amdgcn_readfirstlane(item - sq.tail_first);
+        int ncontrib = 0;
+        const float *pbase = sp.part;
+        int32x4 mine{};
+        if (partial) {
+            // the item's pieces belong to workgroups b0 .. b0 + P - 1, in stage order
+            const int b0 = (int)(t_split * (unsigned)sq.S / sp.piece);
+            ncontrib = sp.maxc;
+            pbase = sp.part + (long long)t_split * sp.maxc * sp.part_floats;
+            mine = make_rsrc_uniform(pbase + (long long)((int)blockIdx.x - b0) * sp.part_floats,
+                                     (unsigned)sp.part_floats * 4u);
         }
+        out_tiles([&](int t, int v, int k_out, const TileIdx &ti, const float *yy) {
+            if (!partial) {
+                store(ti, k_out, yy, whole_of(ti));
+            } else {
+#pragma unroll
+                for (int e = 0; e < MM; e += 4)
+                    buffer_store_f32x4(floatx4{yy[e], yy[e + 1], yy[e + 2], yy[e + 3]}, mine, vlane,
+                                       poff(t, v) + e * 4u, kDeviceCoherent);
+            }
+        });
+        if (partial) {
+            if constexpr (G == 0) {
+                unsigned *written = skc, *decided = skc + 1, *flag = skc + 2;
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's partial is stored
+                signal_wave(written);
+                if (kbl == 0) {
+                    wait_at_least(written, (unsigned)KBW * (nsk + 1));
+                    if (lane == 0) {
+                        const unsigned old = __hip_atomic_fetch_add(sp.cnt + t_split, 1u, __ATOMIC_RELAXED,
+                                                                    __HIP_MEMORY_SCOPE_AGENT);
+                        const unsigned is_last = (old + 1 == (unsigned)ncontrib) ? 1u : 0u;
+                        if (is_last) __hip_atomic_store(sp.cnt + t_split, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        flag[nsk & 1u] = is_last;
+                    }
+                    signal_wave(decided);
+                }
+                wait_at_least(decided, nsk + 1);
+                if (__builtin_amdgcn_readfirstlane(flag[nsk & 1u]) != 0) sum_partials(pbase, ncontrib);
+            }
+            ++nsk;
+        }
+
+        // next segment's first operands are in wa (loaded as step nsteps)
     }
-}
-
-// Items of a persistent workgroup: first + i * stride, i < count.  Items are
-// numbered with the output-channel group fastest; each XCD takes one contiguous
-// range of them and its workgroups take items from it round-robin (workgroup b
-// runs on XCD b % 8 as its (b / 8)-th workgroup), so the workgroups of an XCD
-// work on neighbouring items at any time.
-struct ItemRange {
-    int first, stride, count;
-};
-
-__device__ __forceinline__ ItemRange item_range(int n_items) {
-    constexpr int kXcds = 8;
-    const int nwg = gridDim.x;
-    const int xcd = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
-    const int per = nwg / kXcds, extra = nwg % kXcds;
-    const int wg_on_xcd = per + (xcd < extra ? 1 : 0);
-    const int wg_before = xcd * per + (xcd < extra ? xcd : extra);
-    const int xcd_first = (int)((long long)n_items * wg_before / nwg);
-    const int xcd_end = (int)((long long)n_items * (wg_before + wg_on_xcd) / nwg);
-    ItemRange r;
-    r.first = xcd_first + j;
-    r.stride = wg_on_xcd;
-    r.count = r.first < xcd_end ? (xcd_end - r.first + r.stride - 1) / r.stride : 0;
-    return r;
 }
 
 // Persistent warp-specialised fused kernel: one workgroup per compute unit
 // (register and LDS use allow one).  Items (tile group, output-channel group)
-// are numbered with the output-channel group fastest; each XCD takes one
-// contiguous range of items and its workgroups take items from it round-robin,
-// so at any time the workgroups of an XCD work on neighbouring items: the groups
-// that re-read one tile group's input, and the tile groups whose input tiles
-// share halo rows and columns, find those in the XCD's L2.  Each workgroup runs
-// its items' stages as one sequence, so the next item's first input tiles load
-// and transform while the consumers finish the current item's output transform
-// and stores.
+// are numbered with the output-channel group fastest; the whole items of a
+// workgroup come from one contiguous range per XCD, taken round-robin by its
+// workgroups, so at any time the workgroups of an XCD work on neighbouring items:
+// the groups that re-read one tile group's input, and the tile groups whose input
+// tiles share halo rows and columns, find those in the XCD's L2.  The remaining
+// items are split stage-wise across all workgroups (WsSeq).  Each workgroup runs
+// its stages as one sequence, so the next item's first input tiles load and
+// transform while the consumers finish the current item's output transform and
+// stores.
 template <int M, int TB, int FS, bool VX>
 __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__ x,
                                                        const floatx4 *__restrict__ wt,
                                                        float *__restrict__ y, Geometry g, int vec,
-                                                       int n_kgroups, int n_items) {
+                                                       int n_kgroups, int n_items, WsSplit sp) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB;
     constexpr int CC = 256 / R;
@@ -883,23 +1093,25 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     constexpr int NSLOT = ws_slots<M>();
     // float4s of the combine slots and the pair counters (FS = 2)
     constexpr int COMB = FS == 1 ? 0 : 2 * M * M * 64 / 4 + 1;
-    constexpr int RING = (2 * NSLOT + 3) / 4;  // float4s of the ring counters
+    constexpr int NCNT = 2 * NSLOT + 4;        // ring counters, then split-output counters
+    constexpr int RING = (NCNT + 3) / 4;        // float4s of the counters
     __shared__ floatx4 lds[NSLOT * BUF + COMB + RING];
     float *comb = reinterpret_cast<float *>(lds + NSLOT * BUF);
     unsigned *pairc = FS == 2 ? reinterpret_cast<unsigned *>(comb + 2 * M * M * 64) : nullptr;
     unsigned *ring = reinterpret_cast<unsigned *>(lds + NSLOT * BUF + COMB);  // fill counts, then drain counts
+    unsigned *skc = ring + 2 * NSLOT;  // split outputs: written, decided, flag[2]
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int lane = tid & 63;
-    if (tid < 2 * NSLOT) ring[tid] = 0u;
+    if (tid < NCNT) ring[tid] = 0u;
     if (FS == 2 && tid >= 64 && tid < 68) pairc[tid - 64] = 0u;
     __syncthreads();
-    const ItemRange ir = item_range(n_items);
-    const int first = ir.first, stride = ir.stride, count = ir.count;
     const long long HW = (long long)g.H * g.W;
     const int stages = (g.C + CC - 1) / CC;
-    const int nrounds = count * stages;  // stages this workgroup processes
+    WsSeq sq;
+    sq.init(sp, n_items, stages);
+    const int nrounds = sq.length();  // stages this workgroup processes
 
     if (wave >= 4) {
         // ---------------- producer: load + input transform -> LDS ----------------
@@ -909,18 +1121,23 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         // VX: row-vector loads with DPP halo exchange; otherwise one load per element
         using Loader = typename std::conditional<VX, RowTile<M>, BufTile<M, (M <= 2)>>::type;
         Loader ld;
-        auto init_item = [&](int it) {
-            const TileIdx ti = decode_tile(g, (it / n_kgroups) * R + tr);
-            if constexpr (VX) ld.init(g, ti, cl, lane & 15);
-            else ld.init(g, ti, cl);
-        };
+        int cur_item = -1;
+        // cursors of the stage being loaded (PD ahead) and of the stage transformed
+        WsSeq::Cursor cl_load = sq.start(), cl_proc = sq.start();
         const bool maskcols = (g.W % M) != 0;
         const unsigned xbytes = (unsigned)((long long)g.N * g.C * HW * 4);
         const bool ctail = (g.C % CC) != 0;
-        // load stage r of the sequence (item first + (r / stages) * stride, channel stage r % stages)
-        auto load_stage = [&](int r, float *d, unsigned &fl) {
-            const int st = r % stages;
-            if (st == 0) init_item(first + (r / stages) * stride);
+        // load the next stage of the sequence (its item's tiles are located when the
+        // item changes)
+        auto load_stage = [&](float *d, unsigned &fl) {
+            const int it = cl_load.item, st = cl_load.st;
+            sq.advance(cl_load);
+            if (it != cur_item) {
+                cur_item = it;
+                const TileIdx ti = decode_tile(g, (it / n_kgroups) * R + tr);
+                if constexpr (VX) ld.init(g, ti, cl, lane & 15);
+                else ld.init(g, ti, cl);
+            }
             const long long cbase = (long long)st * CC * HW;
             const int32x4 rs = make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4));
             if constexpr (VX) {
@@ -936,17 +1153,17 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         // flight where registers allow (m <= 4), else PD = 1.
         constexpr int PD = (M <= 4) ? 2 : 1;
         // The loads of round r + PD are issued unconditionally (past the last stage
-        // they read tiles of items beyond this workgroup's, or nothing, at offsets
-        // outside the buffer), so that the wait for a stage's data never has to
-        // cover loads issued after it.
+        // they address tiles outside every image: no memory access), so that the
+        // wait for a stage's data never has to cover loads issued after it.
         auto round = [&](int r, float *dcur, unsigned fcur, float *dnext, unsigned &fnext) {
-            load_stage(r + PD, dnext, fnext);
+            load_stage(dnext, fnext);
             if (r < nrounds) {
                 const int slot = r % NSLOT;
                 const unsigned gen = (unsigned)(r / NSLOT);
                 if constexpr (VX) RowTile<M>::finish(dcur, fcur, maskcols);
                 if (gen > 0) wait_at_least(ring + NSLOT + slot, 4u * gen);
-                const int st = r % stages;
+                const int st = cl_proc.st;
+                sq.advance(cl_proc);
                 // channels past C (last stage only, when C % CC != 0) transform zeros
                 if (ctail && st == stages - 1) {
                     asm volatile("");  // keeps this a branch instead of selects run every stage
@@ -966,24 +1183,24 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         if constexpr (PD == 1) {
             float d0[T2], d1[T2];
             unsigned f0 = 0, f1 = 0;
-            load_stage(0, d0, f0);
-            for (; r + 1 <= nrounds; r += 2) {
+            load_stage(d0, f0);
+            for (; r + 1 < nrounds; r += 2) {
                 round(r, d0, f0, d1, f1);
                 round(r + 1, d1, f1, d0, f0);
             }
-            if (r <= nrounds) round(r, d0, f0, d1, f1);
+            if (r < nrounds) round(r, d0, f0, d1, f1);
         } else {
             float d0[T2], d1[T2], d2[T2];
             unsigned f0 = 0, f1 = 0, f2 = 0;
-            load_stage(0, d0, f0);
-            load_stage(1, d1, f1);
-            for (; r + 2 <= nrounds; r += 3) {
+            load_stage(d0, f0);
+            load_stage(d1, f1);
+            for (; r + 2 < nrounds; r += 3) {
                 round(r, d0, f0, d2, f2);
                 round(r + 1, d1, f1, d0, f0);
                 round(r + 2, d2, f2, d1, f1);
             }
-            if (r <= nrounds) round(r, d0, f0, d2, f2);
-            if (r + 1 <= nrounds) round(r + 1, d1, f1, d0, f0);
+            if (r < nrounds) round(r, d0, f0, d2, f2);
+            if (r + 1 < nrounds) round(r + 1, d1, f1, d0, f0);
         }
         return;
     }
@@ -991,10 +1208,10 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     // ---------------- consumers ----------------
     const int kbl = wave / FS;
     if constexpr (FS == 1) {
-        ws_consume<M, TB, 1, 0>(lds, comb, pairc, ring, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+        ws_consume<M, TB, 1, 0>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
     } else {
-        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, pairc, ring, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
-        else ws_consume<M, TB, FS, 1>(lds, comb, pairc, ring, wt, y, g, first, stride, count, n_kgroups, kbl, lane, stages, vec);
+        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
+        else ws_consume<M, TB, FS, 1>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
     }
 }
 
@@ -1355,24 +1572,78 @@ FusedCfg fused_cfg_default(const Geometry &g) {
     return c;
 }
 
+// Split plan of the warp-specialised kernel (see WsSeq): grid size, whole items
+// per workgroup, the split items and the partial-output buffer they need.
+template <int M, int TB, int FS>
+static SplitInfo ws_split_info(const Geometry &g, int num_cus) {
+    constexpr int R = 16 * TB, CC = 256 / R, KBW = 4 / FS;
+    SplitInfo si{};
+    const int n_tgroups = (g.ntiles + R - 1) / R;
+    si.n_kgroups = (g.Kb + KBW - 1) / KBW;
+    si.n_items = n_tgroups * si.n_kgroups;
+    si.stages = (g.C + CC - 1) / CC;
+    const int cus = num_cus < 1 ? 1 : num_cus;
+    si.nfull = si.n_items / cus;
+    si.grid = si.n_items < cus ? si.n_items : cus;
+    si.part_floats = KBW * TB * 4 * M * M * 64;
+    si.tail_first = si.n_items;  // every item whole unless split below
+    si.n_tail = 0;
+    si.tail_units = 0;
+    si.piece = (unsigned)si.stages;
+    si.maxc = 0;
+    // Split the items of a last, partly filled round into P pieces (P <= 4,
+    // dividing the stages) when at least half of the compute units would idle in
+    // it otherwise.  A piece costs its workgroup a partial-output epilogue
+    // (output transform, device-coherent stores, arrival count) and the last
+    // contributor a sum, which keeps P small; with four or more full rounds the
+    // imbalance is small and items stay whole.
+    constexpr int kMaxPieces = 4, kMaxSplitRounds = 4;
+    const int tail = si.n_items - si.nfull * cus;
+    if (si.nfull >= kMaxSplitRounds || tail == 0 || 2 * tail > cus) return si;
+    int P = cus / tail < kMaxPieces ? cus / tail : kMaxPieces;
+    while (P > 1 && si.stages % P != 0) --P;
+    if (P < 2) return si;
+    si.tail_first = si.nfull * cus;
+    si.n_tail = tail;
+    si.piece = (unsigned)(si.stages / P);
+    si.tail_units = (unsigned)tail * (unsigned)si.stages;
+    si.maxc = P;
+    si.grid = si.nfull > 0 ? cus : tail * P;
+    return si;
+}
+
+SplitInfo fused_split_info(const Geometry &g, const FusedCfg &cfg) {
+    if (cfg.schedule != kSchedSpecialised) return SplitInfo{};
+    switch (g.m) {
+        case 2: return ws_split_info<2, 2, 1>(g, cfg.num_cus);
+        case 4: return ws_split_info<4, 1, 1>(g, cfg.num_cus);
+        default: return ws_split_info<6, 1, 2>(g, cfg.num_cus);
+    }
+}
+
 template <int M, int TB, int FS>
 static void launch_ws_t(const Geometry &g, const float *x, const float *wt, float *y, bool vec,
-                        int num_cus, hipStream_t s) {
-    constexpr int KBW = 4 / FS;
-    const int n_tgroups = (g.ntiles + 16 * TB - 1) / (16 * TB);
-    const int n_kgroups = (g.Kb + KBW - 1) / KBW;
-    const int n_items = n_tgroups * n_kgroups;
-    const int nwg = n_items < num_cus ? n_items : num_cus;
-    dim3 block(512), grid((unsigned)nwg);
+                        int num_cus, const SplitBuffers &sb, hipStream_t s) {
+    const SplitInfo si = ws_split_info<M, TB, FS>(g, num_cus);
+    WsSplit sp;
+    sp.n_whole = si.tail_first;
+    sp.tail_first = si.tail_first;
+    sp.tail_units = si.tail_units;
+    sp.piece = si.piece;
+    sp.part = sb.part;
+    sp.cnt = sb.cnt;
+    sp.maxc = si.maxc;
+    sp.part_floats = si.part_floats;
+    dim3 block(512), grid((unsigned)si.grid);
     // row-vector input loads need every row start aligned to the vector width
     const unsigned vw = (M == 4) ? 16u : 8u;
     const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
     if (vx)
         hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, true>), grid, block, 0, s, x,
-                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_kgroups, n_items);
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, si.n_kgroups, si.n_items, sp);
     else
         hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, false>), grid, block, 0, s, x,
-                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, n_kgroups, n_items);
+                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, si.n_kgroups, si.n_items, sp);
 }
 
 template <int M, int TB>
@@ -1414,7 +1685,7 @@ static void launch_fused_t(const Geometry &g, int waves, const float *x, const f
 }
 
 hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, const float *wt,
-                        float *y, hipStream_t s) {
+                        float *y, const SplitBuffers &sb, hipStream_t s) {
     if (!fused_cfg_supported(g.m, cfg)) return hipErrorInvalidValue;
     const uintptr_t ya = reinterpret_cast<uintptr_t>(y);
     const bool vec = (g.m == 4) ? (g.W % 4 == 0 && ya % 16 == 0) : (g.W % 2 == 0 && ya % 8 == 0);
@@ -1424,9 +1695,9 @@ hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, 
     }
     if (cfg.schedule == kSchedSpecialised) {
         switch (g.m) {
-            case 2: launch_ws_t<2, 2, 1>(g, x, wt, y, vec, cfg.num_cus, s); break;
-            case 4: launch_ws_t<4, 1, 1>(g, x, wt, y, vec, cfg.num_cus, s); break;
-            default: launch_ws_t<6, 1, 2>(g, x, wt, y, vec, cfg.num_cus, s); break;
+            case 2: launch_ws_t<2, 2, 1>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
+            case 4: launch_ws_t<4, 1, 1>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
+            default: launch_ws_t<6, 1, 2>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
         }
         return hipGetLastError();
     }

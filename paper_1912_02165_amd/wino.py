@@ -38,6 +38,7 @@ SIGNATURES = {
 
 
 WINO_SCHED_AUTO, WINO_SCHED_SHARED, WINO_SCHED_PER_WAVE = 0, 1, 2
+WINO_SCHED_SPECIALISED, WINO_SCHED_PERSISTENT = 3, 4
 
 
 class WinoTuning(ctypes.Structure):
