@@ -735,33 +735,52 @@ struct WsSplit {
 
 struct WsSeq {
     int first, stride, nfull;  // whole items first + i * stride, i < nfull
-    unsigned u0, u1;           // split units [u0, u1)
     int S;                     // stages per item
-    int tail_first, n_items;
+    int n_items;
+    int titem, tsb, tse;       // the piece of a split item, stages [tsb, tse) (none if equal)
+    int nseg;                  // segments: nfull whole items, then the piece
 
-    __device__ __forceinline__ void init(const WsSplit &sp, int n_items_, int stages) {
+    __device__ __forceinline__ void init(const WsSplit &sp, int n_items_, int stages, bool split) {
         S = stages;
         n_items = n_items_;
         const ItemRange ir = item_range(sp.n_whole);
         first = ir.first;
         stride = ir.stride;
         nfull = ir.count;
-        tail_first = sp.tail_first;
+        // workgroup b's piece is split units [b*L, b*L + L): pieces never straddle items
         const unsigned long long a = (unsigned long long)blockIdx.x * sp.piece;
-        u0 = (unsigned)(a < sp.tail_units ? a : sp.tail_units);
-        u1 = (unsigned)(a + sp.piece < sp.tail_units ? a + sp.piece : sp.tail_units);
+        titem = n_items;
+        tsb = tse = 0;
+        if (split && a < sp.tail_units) {
+            const unsigned t = (unsigned)a / (unsigned)S;
+            titem = sp.tail_first + (int)t;
+            tsb = (int)((unsigned)a - t * (unsigned)S);
+            tse = tsb + (int)sp.piece;
+        }
+        nseg = nfull + (tse > tsb ? 1 : 0);
     }
-    __device__ __forceinline__ int length() const { return nfull * S + (int)(u1 - u0); }
-    __device__ __forceinline__ int segments() const {
-        return nfull + (u1 > u0 ? (int)((u1 - 1) / (unsigned)S - u0 / (unsigned)S + 1) : 0);
+    __device__ __forceinline__ int length() const { return nfull * S + (tse - tsb); }
+    __device__ __forceinline__ int segments() const { return nseg; }
+    // segment k: item and its stages [sb, se); k past the end repeats the last one
+    __device__ __forceinline__ void segment(int k, int &item, int &sb, int &se) const {
+        k = k < nseg ? k : nseg - 1;
+        if (k < nfull) {
+            item = first + k * stride;
+            sb = 0;
+            se = S;
+        } else {
+            item = titem;
+            sb = tsb;
+            se = tse;
+        }
     }
-    // A walker over the sequence, one stage at a time (no divisions per stage).
+    // A walker over the sequence, one stage at a time.
     struct Cursor {
         int k, item, st, se;
     };
     __device__ __forceinline__ Cursor start() const {
         Cursor c{0, n_items, 0, 1};
-        if (segments() > 0) {
+        if (nseg > 0) {
             int sb;
             segment(0, c.item, sb, c.se);
             c.st = sb;
@@ -771,7 +790,7 @@ struct WsSeq {
     // next stage; past the end, an item that does not exist
     __device__ __forceinline__ void advance(Cursor &c) const {
         if (++c.st < c.se) return;
-        if (++c.k < segments()) {
+        if (++c.k < nseg) {
             int sb;
             segment(c.k, c.item, sb, c.se);
             c.st = sb;
@@ -781,28 +800,11 @@ struct WsSeq {
             c.se = 1;
         }
     }
-    // segment k: item and its stages [sb, se); k past the end repeats the last one
-    __device__ __forceinline__ void segment(int k, int &item, int &sb, int &se) const {
-        const int ns = segments();
-        k = k < ns ? k : ns - 1;
-        if (k < nfull) {
-            item = first + k * stride;
-            sb = 0;
-            se = S;
-        } else {
-            const unsigned t = u0 / (unsigned)S + (unsigned)(k - nfull);
-            const unsigned lo = t * (unsigned)S > u0 ? t * (unsigned)S : u0;
-            const unsigned hi = (t + 1) * (unsigned)S < u1 ? (t + 1) * (unsigned)S : u1;
-            item = tail_first + (int)t;
-            sb = (int)(lo - t * (unsigned)S);
-            se = (int)(hi - t * (unsigned)S);
-        }
-    }
 };
 
 // Consumer of the persistent warp-specialised kernel: the workgroup's segments,
 // as one continuous sequence of stages shared with the producers.
-template <int M, int TB, int FS, int G>
+template <int M, int TB, int FS, int G, bool SPLIT>
 __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsigned *pairc, unsigned *ring,  // shared memory, written by other waves
                                            unsigned *skc,
                                            const floatx4 *__restrict__ wt, float *__restrict__ y,
@@ -1021,8 +1023,8 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
         // reproducible) and stores y.  Partials are written and read with
         // device-coherent accesses; a writer's stores have completed before its
         // arrival is counted.
-        const bool partial = !(sb == 0 && se == sq.S);
-        const unsigned t_split = (unsigned)__builtin_amdgcn_readfirstlane(item - sq.tail_first);
+        const bool partial = SPLIT && !(sb == 0 && se == sq.S);
+        const unsigned t_split = (unsigned)__builtin_amdgcn_readfirstlane(item - sp.tail_first);
         int ncontrib = 0;
         const float *pbase = sp.part;
         int32x4 mine{};
@@ -1081,7 +1083,7 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
 // its stages as one sequence, so the next item's first input tiles load and
 // transform while the consumers finish the current item's output transform and
 // stores.
-template <int M, int TB, int FS, bool VX>
+template <int M, int TB, int FS, bool VX, bool SPLIT>
 __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__ x,
                                                        const floatx4 *__restrict__ wt,
                                                        float *__restrict__ y, Geometry g, int vec,
@@ -1110,7 +1112,7 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     const long long HW = (long long)g.H * g.W;
     const int stages = (g.C + CC - 1) / CC;
     WsSeq sq;
-    sq.init(sp, n_items, stages);
+    sq.init(sp, n_items, stages, SPLIT);
     const int nrounds = sq.length();  // stages this workgroup processes
 
     if (wave >= 4) {
@@ -1208,10 +1210,10 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     // ---------------- consumers ----------------
     const int kbl = wave / FS;
     if constexpr (FS == 1) {
-        ws_consume<M, TB, 1, 0>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
+        ws_consume<M, TB, 1, 0, SPLIT>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
     } else {
-        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
-        else ws_consume<M, TB, FS, 1>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
+        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0, SPLIT>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
+        else ws_consume<M, TB, FS, 1, SPLIT>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
     }
 }
 
@@ -1638,12 +1640,19 @@ static void launch_ws_t(const Geometry &g, const float *x, const float *wt, floa
     // row-vector input loads need every row start aligned to the vector width
     const unsigned vw = (M == 4) ? 16u : 8u;
     const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
-    if (vx)
-        hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, true>), grid, block, 0, s, x,
-                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, si.n_kgroups, si.n_items, sp);
-    else
-        hipLaunchKernelGGL((fused_ws_kernel<M, TB, FS, false>), grid, block, 0, s, x,
-                           reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0, si.n_kgroups, si.n_items, sp);
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, grid, block, 0, s, x, reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0,
+                           si.n_kgroups, si.n_items, sp);
+    };
+    // layers whose items all stay whole run an instantiation without the split path
+    const bool split = si.n_tail > 0;
+    if (vx) {
+        if (split) go(fused_ws_kernel<M, TB, FS, true, true>);
+        else go(fused_ws_kernel<M, TB, FS, true, false>);
+    } else {
+        if (split) go(fused_ws_kernel<M, TB, FS, false, true>);
+        else go(fused_ws_kernel<M, TB, FS, false, false>);
+    }
 }
 
 template <int M, int TB>
