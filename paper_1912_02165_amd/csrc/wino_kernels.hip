@@ -722,6 +722,16 @@ __device__ __forceinline__ ItemRange item_range(int n_items) {
 // segments, one per item it works on; a piece of a split item yields a partial
 // output, and the partial outputs of an item are added by whichever of its P
 // contributors finishes last.
+// Item numbering of the warp-specialised kernel: with KM false the output-channel
+// group varies fastest (items = tile groups x groups, the groups of one tile group
+// adjacent: its input tiles are shared in L2); with KM true the tile group varies
+// fastest (the tile groups of one output-channel group adjacent: its transformed
+// kernels are shared in L2).  n_inner is the count of the fastest index.
+template <bool KM>
+__device__ __forceinline__ int item_tgroup(int it, int n_inner) { return KM ? it % n_inner : it / n_inner; }
+template <bool KM>
+__device__ __forceinline__ int item_kgroup(int it, int n_inner) { return KM ? it / n_inner : it % n_inner; }
+
 struct WsSplit {
     int n_whole;          // items distributed whole (item_range over the first n_whole)
     int tail_first;       // first split item
@@ -804,12 +814,12 @@ struct WsSeq {
 
 // Consumer of the persistent warp-specialised kernel: the workgroup's segments,
 // as one continuous sequence of stages shared with the producers.
-template <int M, int TB, int FS, int G, bool SPLIT>
+template <int M, int TB, int FS, int G, bool SPLIT, bool KM>
 __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsigned *pairc, unsigned *ring,  // shared memory, written by other waves
                                            unsigned *skc,
                                            const floatx4 *__restrict__ wt, float *__restrict__ y,
                                            const Geometry &g, const WsSeq &sq, const WsSplit &sp,
-                                           int n_kgroups, int kbl, int lane, int vec) {
+                                           int n_inner, int kbl, int lane, int vec) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB, CC = 256 / R, SS = CC / 4, BUF = F4 * CC * R;
     constexpr int NSLOT = ws_slots<M>();
@@ -842,7 +852,7 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
     static_assert(MM % 4 == 0, "output tiles are whole float4s");
     const unsigned vlane = (unsigned)lane * MM * 4u;
     auto poff = [&](int t, int v) { return (unsigned)((((kbl * TB + t) * 4 + v) * 64) * MM) * 4u; };
-    auto wbase = [&](int it) { return (unsigned)(((it % n_kgroups) * KBW + kbl) * g.Cs) * SB; };
+    auto wbase = [&](int it) { return (unsigned)((item_kgroup<KM>(it, n_inner) * KBW + kbl) * g.Cs) * SB; };
     auto wload = [&](unsigned soff, int lf) { return buffer_load_f32x4(wrs, vo, soff + gm.f4[lf] * 1024u, 0); };
     const int last = g.Cs - 1;
     const int nseg = sq.segments();
@@ -921,8 +931,8 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
 
         // Output transform Y = A^T Mm A per (output channel, tile), clipped to H x W,
         // into yy; emit(t, v, k, ti, yy) consumes each finished output tile.
-        const int tile0 = (item / n_kgroups) * R;
-        const int kb = (item % n_kgroups) * KBW + kbl;
+        const int tile0 = item_tgroup<KM>(item, n_inner) * R;
+        const int kb = item_kgroup<KM>(item, n_inner) * KBW + kbl;
         auto out_tiles = [&](auto emit) {
 #pragma unroll
             for (int t = 0; t < TB; ++t) {
@@ -1083,11 +1093,11 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
 // its stages as one sequence, so the next item's first input tiles load and
 // transform while the consumers finish the current item's output transform and
 // stores.
-template <int M, int TB, int FS, bool VX, bool SPLIT>
+template <int M, int TB, int FS, bool VX, bool SPLIT, bool KM>
 __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__ x,
                                                        const floatx4 *__restrict__ wt,
                                                        float *__restrict__ y, Geometry g, int vec,
-                                                       int n_kgroups, int n_items, WsSplit sp) {
+                                                       int n_inner, int n_items, WsSplit sp) {
     constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
     constexpr int R = 16 * TB;
     constexpr int CC = 256 / R;
@@ -1136,7 +1146,7 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
             sq.advance(cl_load);
             if (it != cur_item) {
                 cur_item = it;
-                const TileIdx ti = decode_tile(g, (it / n_kgroups) * R + tr);
+                const TileIdx ti = decode_tile(g, item_tgroup<KM>(it, n_inner) * R + tr);
                 if constexpr (VX) ld.init(g, ti, cl, lane & 15);
                 else ld.init(g, ti, cl);
             }
@@ -1210,10 +1220,10 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     // ---------------- consumers ----------------
     const int kbl = wave / FS;
     if constexpr (FS == 1) {
-        ws_consume<M, TB, 1, 0, SPLIT>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
+        ws_consume<M, TB, 1, 0, SPLIT, KM>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_inner, kbl, lane, vec);
     } else {
-        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0, SPLIT>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
-        else ws_consume<M, TB, FS, 1, SPLIT>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_kgroups, kbl, lane, vec);
+        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0, SPLIT, KM>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_inner, kbl, lane, vec);
+        else ws_consume<M, TB, FS, 1, SPLIT, KM>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_inner, kbl, lane, vec);
     }
 }
 
@@ -1640,18 +1650,24 @@ static void launch_ws_t(const Geometry &g, const float *x, const float *wt, floa
     // row-vector input loads need every row start aligned to the vector width
     const unsigned vw = (M == 4) ? 16u : 8u;
     const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
+    // Item order: when the transformed kernels outweigh the input (deep layers),
+    // the tile groups of one output-channel group are numbered adjacently, so the
+    // workgroups of an XCD share that group's transformed kernels in L2.
+    const bool km = si.n_kgroups > 1 &&
+                    (double)g.T2 * g.C * g.K > (double)g.N * g.C * g.H * g.W;
+    const int n_inner = km ? si.n_items / si.n_kgroups : si.n_kgroups;
     auto go = [&](auto kern) {
         hipLaunchKernelGGL(kern, grid, block, 0, s, x, reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0,
-                           si.n_kgroups, si.n_items, sp);
+                           n_inner, si.n_items, sp);
     };
     // layers whose items all stay whole run an instantiation without the split path
     const bool split = si.n_tail > 0;
     if (vx) {
-        if (split) go(fused_ws_kernel<M, TB, FS, true, true>);
-        else go(fused_ws_kernel<M, TB, FS, true, false>);
+        if (split) km ? go(fused_ws_kernel<M, TB, FS, true, true, true>) : go(fused_ws_kernel<M, TB, FS, true, true, false>);
+        else km ? go(fused_ws_kernel<M, TB, FS, true, false, true>) : go(fused_ws_kernel<M, TB, FS, true, false, false>);
     } else {
-        if (split) go(fused_ws_kernel<M, TB, FS, false, true>);
-        else go(fused_ws_kernel<M, TB, FS, false, false>);
+        if (split) km ? go(fused_ws_kernel<M, TB, FS, false, true, true>) : go(fused_ws_kernel<M, TB, FS, false, true, false>);
+        else km ? go(fused_ws_kernel<M, TB, FS, false, false, true>) : go(fused_ws_kernel<M, TB, FS, false, false, false>);
     }
 }
 
