@@ -25,6 +25,9 @@ SMALL = [
     (1, 1, 1, 1, 1), (1, 2, 3, 2, 5), (1, 3, 4, 1, 9), (1, 3, 5, 7, 9), (2, 4, 16, 8, 8),
     (1, 5, 17, 13, 11), (3, 8, 20, 17, 23), (2, 37, 45, 29, 35), (2, 16, 33, 30, 31),
     (1, 64, 64, 20, 20), (4, 12, 40, 6, 6), (1, 130, 18, 9, 10),
+    # more output channels than one group and kernels outweighing the input: items
+    # numbered tile-group fastest, most of them split into pieces
+    (1, 32, 128, 8, 8), (2, 20, 96, 13, 6), (1, 9, 200, 5, 5),
 ]
 
 
@@ -130,6 +133,26 @@ def test_three_stage_intermediates(m):
     scale = np.abs(M_ref).max()
     np.testing.assert_allclose(Mf[:, :K, :ntiles], M_ref, rtol=0, atol=1e-5 * scale)
     assert_close(y.cpu().numpy(), direct_conv(x, w), m, "three-stage end to end")
+
+
+@pytest.mark.parametrize("m", (2, 4, 6))
+def test_plan_reused_across_calls(m):
+    """One plan, several calls: split items' arrival counters are back at zero after
+    every call, so each call is correct and bitwise equal to the first."""
+    N, C, K, H, W = 2, 24, 80, 14, 15
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=40 + m)
+    ref = direct_conv(x, w)
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    ys = []
+    with wc.Plan(N, C, K, H, W, m) as p:
+        for _ in range(3):
+            y = torch.full((N, K, H, W), float("nan"), device="cuda")
+            p.run(xd, wd, y)
+            ys.append(y)
+        torch.cuda.synchronize()
+    for y in ys:
+        assert torch.equal(y, ys[0])
+    assert_close(ys[0].cpu().numpy(), ref, m, f"reused plan F({m})")
 
 
 @pytest.mark.parametrize("algo", ALGOS)
