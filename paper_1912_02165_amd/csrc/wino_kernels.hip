@@ -217,12 +217,16 @@ struct BufTile {
 // horizontally adjacent tiles of the same channel (tiles are numbered along
 // rows), and the T = m + 2 columns of a tile's row are its own m columns plus one
 // halo column on each side, which are the neighbours' own edge columns.  So each
-// lane loads only its own m columns of a row with one vector load and takes the
+// lane loads only its own m columns of a row with vector loads and takes the
 // halo columns from lanes l-1 and l+1 with DPP row shifts.  A tile in the first
-// (last) column of tiles has zero padding on its left (right); a lane at the
-// edge of a 16-lane row whose neighbour tile is in another group fetches that
-// one column itself.  The vector loads need rows aligned to the vector width
-// (checked on the host).
+// (last) column of tiles has zero padding on its left (right).
+//
+// The two halo columns that no lane of the DPP row owns (left of its first tile,
+// right of its last) take 2T elements, which the row fetches with ONE load: lane
+// 15-2a loads element a of the left column and lane 14-2a element a of the right
+// one (a < T <= 8).  A rotation of the row by 2a+1 lanes then brings element a of
+// the left column to lane 0 and of the right column to lane 15, where the row
+// shifts (which leave the edge lane's own value in place) pass it on.
 __device__ __forceinline__ float dpp_from_left(float v) {   // lane l gets lane l-1 (0 at row start)
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
                                                                  0x111, 0xf, 0xf, true));
@@ -231,17 +235,62 @@ __device__ __forceinline__ float dpp_from_right(float v) {  // lane l gets lane 
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
                                                                  0x101, 0xf, 0xf, true));
 }
+// lane l gets lane l-1; lane 0 of each row keeps `edge`
+__device__ __forceinline__ float dpp_from_left_or(float edge, float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, edge),
+                                                                 __builtin_bit_cast(int, v), 0x111,
+                                                                 0xf, 0xf, false));
+}
+// lane l gets lane l+1; lane 15 of each row keeps `edge`
+__device__ __forceinline__ float dpp_from_right_or(float edge, float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, edge),
+                                                                 __builtin_bit_cast(int, v), 0x101,
+                                                                 0xf, 0xf, false));
+}
+// lane l gets lane (l - S) mod 16 of its row
+template <int S>
+__device__ __forceinline__ float dpp_rotate(float v) {
+    static_assert(S >= 1 && S <= 15, "row rotation by 1..15 lanes");
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                                 0x120 + S, 0xf, 0xf, true));
+}
+
+// First and last tile of the 16-lane DPP row that holds tile t0 + tr of a task of
+// 16*TB tiles starting at t0.  Each candidate is decoded from a wave-uniform
+// index (on the scalar unit) and the lane picks its row's.
+template <int TB>
+__device__ __forceinline__ void row_edges(const Geometry &g, int t0, int tr, TileIdx &rf, TileIdx &rl) {
+    rf = decode_tile(g, t0);
+    rl = decode_tile(g, t0 + 15);
+#pragma unroll
+    for (int k = 1; k < TB; ++k) {
+        const TileIdx f = decode_tile(g, t0 + 16 * k), l = decode_tile(g, t0 + 16 * k + 15);
+        if ((tr >> 4) == k) {
+            rf = f;
+            rl = l;
+        }
+    }
+}
 
 template <int M>
 struct RowTile {
     static constexpr int T = M + 2;
+    static_assert(T <= 8, "2T halo elements per 16-lane row");
     unsigned roff[T];   // byte offset of column 0 of input row a (>= 2^31 if outside)
     unsigned own;       // byte offset of the tile's first own column, tx*M*4
+    unsigned hoff;      // byte offset of the row's halo element this lane fetches
     bool first, last;   // tile in the first / last column of tiles: halo is padding
-    bool fetch_l, fetch_r;
     unsigned ownok;     // bit j: own column j lies inside the image
 
-    __device__ __forceinline__ void init(const Geometry &g, const TileIdx &t, int lane_c, int lane16) {
+    // Halo element of lane `lane16`: side (left for odd lanes) and row a.
+    static __device__ __forceinline__ bool halo_left(int lane16) { return (lane16 & 1) != 0; }
+    static __device__ __forceinline__ int halo_row(int lane16) {
+        return halo_left(lane16) ? (15 - lane16) >> 1 : (14 - lane16) >> 1;
+    }
+
+    // t: this lane's tile; rfirst, rlast: the first and last tile of its DPP row.
+    __device__ __forceinline__ void init(const Geometry &g, const TileIdx &t, const TileIdx &rfirst,
+                                         const TileIdx &rlast, int lane_c, int lane16) {
         const unsigned base = (unsigned)(((long long)t.n * g.C + lane_c) * g.H * g.W) * 4u;
 #pragma unroll
         for (int a = 0; a < T; ++a) {
@@ -251,58 +300,75 @@ struct RowTile {
         own = (unsigned)(t.tx * M) * 4u;
         first = t.tx == 0;
         last = t.tx == g.TW - 1;
-        fetch_l = lane16 == 0 && !first;
-        fetch_r = lane16 == 15 && !last;
         ownok = 0u;
 #pragma unroll
         for (int j = 0; j < M; ++j)
             if (t.tx * M + j < g.W) ownok |= 1u << j;
+        // column left of the first tile / right of the last; outside the image
+        // (padding) it reads as 0
+        const bool left = halo_left(lane16);
+        const TileIdx edge = left ? rfirst : rlast;
+        const int a = halo_row(lane16);
+        const int h = edge.ty * M - 1 + a;
+        const int w = left ? edge.tx * M - 1 : edge.tx * M + M;
+        hoff = kOutside;
+        if (a < T && edge.ok && h >= 0 && h < g.H && w >= 0 && w < g.W)
+            hoff = (unsigned)((((long long)edge.n * g.C + lane_c) * g.H + h) * g.W + w) * 4u;
     }
 
     // Issues the loads of one tile without waiting for them: row a of d receives
-    // [fetched halo, own columns, -]; the halo taken from the neighbouring lanes
-    // and the masks are applied by finish(), once the data has arrived, so that
-    // loads can run several stages ahead.
+    // [-, own columns, -] and d[0] the lane's halo element; the halo exchange and
+    // the masks are applied by finish(), once the data has arrived, so that loads
+    // can run several stages ahead.
     __device__ __forceinline__ void issue(int32x4 r, float *d) const {
 #pragma unroll
         for (int a = 0; a < T; ++a) {
-            // Own columns with one vector load (two 8-byte loads and one more for
-            // m = 6).  roff is below 2^31 or exactly 2^31 and own + 4*M is below
-            // 2^31, so the offsets never wrap.
+            // Own columns with one vector load for m = 2, 4 and two (4 + 2) for
+            // m = 6 (rows 8-byte aligned).  roff is below 2^31 or exactly 2^31 and
+            // own + 4*M is below 2^31, so the offsets never wrap.
             const unsigned base = roff[a] + own;
             if constexpr (M == 4) {
                 const floatx4 q = buffer_load_f32x4(r, base, 0, 0);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) d[a * T + 1 + j] = q[j];
-            } else {
+            } else if constexpr (M == 6) {
+                const floatx4 q = buffer_load_f32x4(r, base, 0, 0);
+                const floatx2 q2 = buffer_load_f32x2(r, base + 16u, 0, 0);
 #pragma unroll
-                for (int j = 0; j < M; j += 2) {
-                    const floatx2 q = buffer_load_f32x2(r, base + 4u * j, 0, 0);
-                    d[a * T + 1 + j] = q[0];
-                    d[a * T + 2 + j] = q[1];
-                }
+                for (int j = 0; j < 4; ++j) d[a * T + 1 + j] = q[j];
+                d[a * T + 5] = q2[0];
+                d[a * T + 6] = q2[1];
+            } else {
+                static_assert(M == 2, "m = 2, 4 or 6");
+                const floatx2 q = buffer_load_f32x2(r, base, 0, 0);
+                d[a * T + 1] = q[0];
+                d[a * T + 2] = q[1];
             }
-            // the one halo column a row-edge lane fetches itself (left for the first
-            // lane of a 16-lane row, right for the last): one load for both
-            d[a * T] = buffer_load_f32(r, fetch_l ? base - 4u : (fetch_r ? base + 4u * M : kOutside), 0, 0);
         }
+        d[0] = buffer_load_f32(r, hoff, 0, 0);
     }
 
     // The per-tile facts finish() needs, packed so they can travel with the data
     // of a stage while the loader moves on to the next item.
     __device__ __forceinline__ unsigned flags() const {
-        return (first ? 1u : 0u) | (last ? 2u : 0u) | (fetch_l ? 4u : 0u) | (fetch_r ? 8u : 0u) | (ownok << 8);
+        return (first ? 1u : 0u) | (last ? 2u : 0u) | (ownok << 8);
+    }
+
+    template <int A = 0>
+    static __device__ __forceinline__ void finish_rows(float *d, float hf, unsigned fl) {
+        if constexpr (A < T) {
+            // element A of the row's outer halo columns, now in lanes 0 and 15
+            const float hv = dpp_rotate<2 * A + 1>(hf);
+            const float ln = dpp_from_left_or(hv, d[A * T + M]);  // left neighbour's last own column
+            const float rn = dpp_from_right_or(hv, d[A * T + 1]);  // right neighbour's first own column
+            d[A * T] = (fl & 1u) ? 0.0f : ln;
+            d[A * T + T - 1] = (fl & 2u) ? 0.0f : rn;
+            finish_rows<A + 1>(d, hf, fl);
+        }
     }
 
     static __device__ __forceinline__ void finish(float *d, unsigned fl, bool maskcols) {
-#pragma unroll
-        for (int a = 0; a < T; ++a) {
-            const float ln = dpp_from_left(d[a * T + M]);  // left neighbour's last own column
-            const float rn = dpp_from_right(d[a * T + 1]);  // right neighbour's first own column
-            const float h = d[a * T];                        // fetched halo, if any
-            d[a * T] = (fl & 1u) ? 0.0f : ((fl & 4u) ? h : ln);
-            d[a * T + T - 1] = (fl & 2u) ? 0.0f : ((fl & 8u) ? h : rn);
-        }
+        finish_rows(d, d[0], fl);
         if (maskcols) {  // own columns past W (W % m != 0)
             asm volatile("");  // keeps this a branch instead of selects run by every tile
 #pragma unroll
@@ -1146,9 +1212,15 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
             sq.advance(cl_load);
             if (it != cur_item) {
                 cur_item = it;
-                const TileIdx ti = decode_tile(g, item_tgroup<KM>(it, n_inner) * R + tr);
-                if constexpr (VX) ld.init(g, ti, cl, lane & 15);
-                else ld.init(g, ti, cl);
+                const int t0 = item_tgroup<KM>(it, n_inner) * R;
+                const TileIdx ti = decode_tile(g, t0 + tr);
+                if constexpr (VX) {
+                    TileIdx rf, rl;
+                    row_edges<TB>(g, t0, tr, rf, rl);
+                    ld.init(g, ti, rf, rl, cl, lane & 15);
+                } else {
+                    ld.init(g, ti, cl);
+                }
             }
             const long long cbase = (long long)st * CC * HW;
             const int32x4 rs = make_rsrc(x + cbase, xbytes - (unsigned)(cbase * 4));
@@ -1291,9 +1363,15 @@ fused_1w_kernel(const float *__restrict__ x, const floatx4 *__restrict__ wt, flo
             const int it = ir.first + (q / stages) * ir.stride;
 #pragma unroll
             for (int n = 0; n < NT; ++n) {
-                const TileIdx ti = decode_tile(g, (it / n_kgroups) * R + tr[n]);
-                if constexpr (VX) ld[n].init(g, ti, cl[n], lane & 15);
-                else ld[n].init(g, ti, cl[n]);
+                const int t0 = (it / n_kgroups) * R;
+                const TileIdx ti = decode_tile(g, t0 + tr[n]);
+                if constexpr (VX) {
+                    TileIdx rf, rl;
+                    row_edges<TB>(g, t0, tr[n], rf, rl);
+                    ld[n].init(g, ti, rf, rl, cl[n], lane & 15);
+                } else {
+                    ld[n].init(g, ti, cl[n]);
+                }
             }
         }
         const long long cbase = (long long)st * CC * HW;
