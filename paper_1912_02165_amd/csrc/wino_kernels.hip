@@ -136,6 +136,8 @@ __device__ floatx4 buffer_load_f32x4(int32x4 rsrc, unsigned voffset, unsigned so
     __asm("llvm.amdgcn.raw.buffer.load.v4f32");
 __device__ void buffer_store_f32x4(floatx4 v, int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
     __asm("llvm.amdgcn.raw.buffer.store.v4f32");
+__device__ void buffer_store_f32x2(floatx2 v, int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.store.v2f32");
 // Cache-policy bit of a buffer access that makes it coherent across the device
 // (the coherence that device-scope atomic loads and stores use).
 constexpr int kDeviceCoherent = 1 << 4;
@@ -633,6 +635,25 @@ __device__ __forceinline__ void store_rows(float *__restrict__ yp, const float *
     }
 }
 
+// The same through a buffer resource over y: the tile's first element at byte
+// offset voff (per lane) + soff (uniform), rows rowb bytes apart (uniform), so the
+// per-row and per-channel steps are scalar adds.
+template <int M>
+__device__ __forceinline__ void store_rows_buf(int32x4 yrs, unsigned voff, unsigned soff, unsigned rowb,
+                                               const float *yy) {
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+        const unsigned so = soff + (unsigned)i * rowb;
+        if constexpr (M == 4) {
+            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, 0);
+        } else {
+#pragma unroll
+            for (int jj = 0; jj < M; jj += 2)
+                buffer_store_f32x2(floatx2{yy[i * M + jj], yy[i * M + jj + 1]}, yrs, voff + 4u * jj, so, 0);
+        }
+    }
+}
+
 // Store one m x m output tile of plane yp (clipped to H x W).  vec: rows may be
 // written with m-float vector stores (16-byte aligned for m = 4, 8-byte for m = 2, 6).
 template <int M>
@@ -896,6 +917,8 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
     static_assert(FS == 1 || T == 8, "frequency split is built for F(6) only");
     constexpr GroupF4<M, FS, G> gm{};
     const long long HW = (long long)g.H * g.W;
+    const int32x4 yrs = make_rsrc(y, (unsigned)((long long)g.N * g.K * HW * 4));
+    const unsigned hwb = (unsigned)(HW * 4), rowb = (unsigned)g.W * 4u;
 
     static_assert(SS % 2 == 0, "channel steps are processed in pairs");
     // Kernel operands alternate between two register sets over channel steps (set
@@ -1043,11 +1066,14 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
                 }
             }
         };
-        auto store = [&](const TileIdx &ti, int k_out, const float *yy, bool whole) {
-            if (whole)
-                store_rows<M>(y + ((long long)ti.n * g.K + k_out) * HW + (long long)ti.ty * M * g.W + ti.tx * M,
-                              yy, g.W);
-            else if (ti.ok && k_out < g.K)
+        // Whole tiles: buffer stores at the byte offset of output channel k_out - v
+        // (per lane, y is below 2^31 bytes) plus v planes (scalar).
+        auto store = [&](const TileIdx &ti, int k_out, int v, const float *yy, bool whole) {
+            if (whole) {
+                const unsigned vb = (unsigned)((((long long)ti.n * g.K + (k_out - v)) * HW +
+                                                (long long)ti.ty * M * g.W + ti.tx * M) * 4);
+                store_rows_buf<M>(yrs, vb, (unsigned)v * hwb, rowb, yy);
+            } else if (ti.ok && k_out < g.K)
                 store_tile<M>(y + ((long long)ti.n * g.K + k_out) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
         };
         // When every tile of the wave lies wholly inside the image and all 16 output
@@ -1087,7 +1113,7 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
                             }
                         }
                     }
-                    store(ti, kb * 16 + (lane >> 4) * 4 + v, yy, whole);
+                    store(ti, kb * 16 + (lane >> 4) * 4 + v, v, yy, whole);
                 }
             }
         };
@@ -1114,7 +1140,7 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
         }
         out_tiles([&](int t, int v, int k_out, const TileIdx &ti, const float *yy) {
             if (!partial) {
-                store(ti, k_out, yy, whole_of(ti));
+                store(ti, k_out, v, yy, whole_of(ti));
             } else {
 #pragma unroll
                 for (int e = 0; e < MM; e += 4)
