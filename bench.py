@@ -13,6 +13,11 @@ three-stage variant's step time on the same layer, and the CPU oracle timed on
 the host cores.
 
     python bench.py [--steps K] [--warmup W] [--layer ID --m M] [--all] [--no-cpu]
+
+--all adds a per-(layer, m, algorithm) table (stderr, and --out): back-to-back step
+time, the median of single calls warm and cold (a 512 MB scratch write before each
+cold call evicts L2 and the Infinity Cache), and the transform-domain kernel time;
+plus, per layer, the m and algorithm a tuned plan picks (algo "tuned").
 """
 
 import argparse
@@ -64,9 +69,29 @@ def measured_traffic(kernel, workload):
     return None
 
 
-def time_pair(layer, m, algo, steps, warmup, x, w):
+def rep_times(p, x, w, y, steps, stream, scratch=None):
+    """Per-call times (ms) of `steps` separate run() calls, each bracketed by its own
+    events; with `scratch`, the buffer is overwritten before every call (outside the
+    events) so that the call finds neither L2 nor the Infinity Cache warm."""
+    import torch
+    times = []
+    for _ in range(steps):
+        if scratch is not None:
+            scratch.fill_(1.0)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        p.run(x, w, y)
+        b.record(stream)
+        b.synchronize()
+        times.append(a.elapsed_time(b))
+    return sorted(times)[len(times) // 2]
+
+
+def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False):
     """Time `steps` steps; returns dict with ms_per_step and the transform-domain
-    kernel's average duration (ms) measured between events on the same stream."""
+    kernel's average duration (ms) measured between events on the same stream.
+    per_call: also the median time of single calls, warm and cold (after a 512 MB
+    scratch write that evicts L2 and the 256 MB Infinity Cache)."""
     import torch
     import paper_1912_02165_amd as wc
     N, C, K, H, W = layer.N, layer.C, layer.K, layer.H, layer.W
@@ -99,8 +124,14 @@ def time_pair(layer, m, algo, steps, warmup, x, w):
         wt_ms = sum(a.elapsed_time(b) for a, b, _ in evs) / steps
         body_ms = sum(b.elapsed_time(c) for _, b, c in evs) / steps
         nt, dflops, tflops = p.info()
-    return {"ms_per_step": ms_step, "weight_transform_ms": wt_ms, "body_ms": body_ms,
-            "direct_flops": dflops, "tdomain_flops": tflops, "tiles": nt}
+        res = {"ms_per_step": ms_step, "weight_transform_ms": wt_ms, "body_ms": body_ms,
+               "direct_flops": dflops, "tdomain_flops": tflops, "tiles": nt}
+        if per_call:
+            res["warm_call_ms_median"] = rep_times(p, x, w, y, steps, stream)
+            scratch = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
+            res["cold_call_ms_median"] = rep_times(p, x, w, y, steps, stream, scratch)
+            del scratch
+    return res
 
 
 def cpu_baseline(layer, budget_s=20.0):
@@ -180,18 +211,33 @@ def main():
         rec["cpu_baseline"] = cpu_baseline(layer)
 
     if args.all:
+        import paper_1912_02165_amd as wc
         rows = []
+        tuned_done = set()
         for lay, mm in workloads.PAIRS:
             xn, wn = workloads.layer_inputs(lay)
             xa, wa = torch.from_numpy(xn).cuda(), torch.from_numpy(wn).cuda()
-            for algo in ("fused", "three_stage"):
-                r = time_pair(lay, mm, algo, args.steps, args.warmup, xa, wa)
-                row = {"workload": lay.tag(mm), "algo": algo, "ms_per_step": r["ms_per_step"],
+            cases = [(mm, "fused", "fused"), (mm, "three_stage", "three_stage")]
+            if lay.id not in tuned_done:
+                # the tile size and algorithm a per-layer tuning picks (timed now)
+                tuned_done.add(lay.id)
+                tp = wc.Plan.tuned(lay.N, lay.C, lay.K, lay.H, lay.W,
+                                   wc.WINO_TUNE_ALL_M | wc.WINO_TUNE_THREE_STAGE)
+                cases.append((tp.m, tp.algo, "tuned"))
+                tp.close()
+            for m_c, algo, label in cases:
+                r = time_pair(lay, m_c, algo, args.steps, args.warmup, xa, wa, per_call=True)
+                row = {"workload": lay.tag(m_c), "algo": label, "ms_per_step": r["ms_per_step"],
                        "eff_tflops": r["direct_flops"] / (r["ms_per_step"] * 1e-3) / 1e12,
+                       "warm_call_ms_median": r["warm_call_ms_median"],
+                       "cold_call_ms_median": r["cold_call_ms_median"],
+                       "eff_tflops_cold": r["direct_flops"] / (r["cold_call_ms_median"] * 1e-3) / 1e12,
                        "body_ms": r["body_ms"],
                        "tdomain_tflops_body": r["tdomain_flops"] / (r["body_ms"] * 1e-3) / 1e12,
                        "mfma_frac_body": r["tdomain_flops"] / (r["body_ms"] * 1e-3) / P_MFMA_F32,
                        "weight_transform_ms": r["weight_transform_ms"]}
+                if label == "tuned":
+                    row["tuned_choice"] = {"m": m_c, "algo": algo}
                 rows.append(row)
                 print(json.dumps(row), file=sys.stderr, flush=True)
             del xa, wa

@@ -1,0 +1,84 @@
+/*
+ * wino_tune.h -- per-layer tuning of the Winograd convolution and its wisdom table.
+ *
+ * Sec. 6 runs one fixed configuration on every layer and notes that tuning the
+ * parameters for each particular layer can only improve the results; Sec. 7
+ * says that tuning is done once and stored in a wisdom file.  Here the tuned
+ * parameter is the tile size m of F(m x m, 3 x 3) (the paper's T = m + 2; the
+ * number of tiles per task is fixed by the matrix-core blocking) and, optionally,
+ * the algorithm (fused or three-stage).  A tuning result is remembered per
+ * (GPU architecture, compute units, N, C, K, H, W, candidate set) in a
+ * process-wide wisdom table that can be written to and read from a text file.
+ *
+ * Wisdom file: text, one entry per line, '#' starts a comment line:
+ *     <arch> <cus> <N> <C> <K> <H> <W> <candidates> <m> <algo> <microseconds>
+ * arch is the device's architecture name (e.g. gfx950), candidates is the
+ * candidate mask in hexadecimal (0x...), algo is 0 (fused) or 1 (three-stage)
+ * and microseconds the measured time of one call.
+ *
+ * Thread safety: the wisdom table is guarded by a lock; plans are as in
+ * wino_conv.h (one stream at a time).
+ */
+#ifndef WINO_TUNE_H
+#define WINO_TUNE_H
+
+#include "wino_conv.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Candidate mask bits: tile sizes, and whether the three-stage algorithm is
+ * also tried at each of them. */
+enum {
+    WINO_TUNE_M2 = 1 << 2,
+    WINO_TUNE_M4 = 1 << 4,
+    WINO_TUNE_M6 = 1 << 6,
+    WINO_TUNE_THREE_STAGE = 1 << 8
+};
+
+/* A plan for the convolution of wino_conv_plan (N x C x H x W input, K output
+ * channels) with the m and algorithm that run fastest on the current device
+ * among the candidates (a nonzero mask of WINO_TUNE_* bits with at least one
+ * WINO_TUNE_M* bit).  If the wisdom table holds the answer it is used directly;
+ * otherwise every candidate is planned and timed here: its kernels transformed
+ * once, then the median of 5 calls of wino_conv_run_pretransformed after 2
+ * warm-up calls, on device buffers of the layer's size that this function
+ * allocates, fills with a constant and frees before returning (synchronous;
+ * needs room for x, y and w beside the largest candidate's workspace).  The
+ * result enters the wisdom table.  chosen_m, chosen_algo and call_us (each may
+ * be NULL) receive the choice and its measured time (0 if it came from the
+ * table without a time).  Returns NULL (see wino_last_error) for bad sizes, a
+ * bad mask, or a failed allocation or launch. */
+wino_plan *wino_conv_plan_tuned(int N, int C, int K, int H, int W, unsigned candidates,
+                                int *chosen_m, int *chosen_algo, double *call_us);
+
+/* The tile size m and algorithm of a plan.  Returns WINO_EINVAL for NULL. */
+int wino_conv_plan_params(const wino_plan *p, int *m, int *algo);
+
+/* Look up an entry: on WINO_OK, *found is 1 and *m, *algo hold the entry, or
+ * *found is 0.  arch is an architecture name as in the file.  Returns
+ * WINO_EINVAL for NULL pointers. */
+int wino_wisdom_lookup(const char *arch, int cus, int N, int C, int K, int H, int W,
+                       unsigned candidates, int *found, int *m, int *algo);
+
+/* Write the table to path (replacing the file).  Returns WINO_EINVAL if the
+ * file cannot be written. */
+int wino_wisdom_save(const char *path);
+
+/* Merge the entries of a wisdom file into the table (an entry replaces one
+ * with the same key).  The file is checked completely first: a malformed line
+ * (wrong field count or an m, algo or size out of range) leaves the table
+ * unchanged and returns WINO_EINVAL naming the line; so does an unreadable
+ * file. */
+int wino_wisdom_load(const char *path);
+
+/* Remove every entry.  Number of entries in the table. */
+void wino_wisdom_clear(void);
+int wino_wisdom_size(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WINO_TUNE_H */

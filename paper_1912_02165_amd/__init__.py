@@ -1,7 +1,7 @@
 """Fused Winograd 3x3 convolution for AMD MI355X (gfx950).
 
 The compute path is the HIP library ``libwino_conv.so`` behind the C ABI of
-``include/wino_conv.h``; ``wino`` is its Python binding and ``workloads`` draws
+``include/wino_conv.h`` and ``include/wino_tune.h``; ``wino`` is its Python binding and ``workloads`` draws
 the seeded synthetic layers.  Importing the package does not load the library;
 the first binding call does, and fails loudly if it is not built.
 """
@@ -12,4 +12,7 @@ from .wino import (  # noqa: F401
     wino_conv_copy_intermediate, wino_conv_destroy, wino_conv_info, wino_conv_intermediate_dims,
     wino_conv_plan, wino_conv_plan_ex, wino_conv_run, wino_conv_run_pretransformed,
     wino_conv_set_weights, wino_conv_workspace_bytes, wino_last_error,
+    WINO_TUNE_ALL_M, WINO_TUNE_M2, WINO_TUNE_M4, WINO_TUNE_M6, WINO_TUNE_THREE_STAGE,
+    wino_conv_plan_params, wino_conv_plan_tuned, wino_wisdom_clear, wino_wisdom_load,
+    wino_wisdom_lookup, wino_wisdom_save, wino_wisdom_size,
 )

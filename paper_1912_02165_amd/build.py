@@ -14,7 +14,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libwino_conv.so")
-SOURCES = [os.path.join(CSRC, "wino_kernels.hip"), os.path.join(CSRC, "wino_api.cpp")]
+SOURCES = [os.path.join(CSRC, "wino_kernels.hip"), os.path.join(CSRC, "wino_api.cpp"),
+           os.path.join(CSRC, "wino_tune.cpp")]
 ARCH = "gfx950"
 
 

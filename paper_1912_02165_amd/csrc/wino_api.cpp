@@ -2,6 +2,7 @@
 // plan construction, argument checks, workspace ownership and launch order.
 #include "wino_conv.h"
 #include "wino_internal.h"
+#include "wino_tune.h"
 
 #include <hip/hip_runtime.h>
 
@@ -186,6 +187,16 @@ int check_io(const wino_plan *p, const float *x, float *y, hipStream_t s) {
 
 }  // namespace
 
+// Error reporting for the other translation units of the library.
+void wino::set_error(const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+}
+
 extern "C" {
 
 const char *wino_last_error(void) { return g_err.c_str(); }
@@ -298,6 +309,16 @@ oom:
             total_bytes);
     wino_conv_destroy(p);
     return nullptr;
+}
+
+int wino_conv_plan_params(const wino_plan *p, int *m, int *algo) {
+    if (!p) {
+        set_err("plan is NULL");
+        return WINO_EINVAL;
+    }
+    if (m) *m = p->g.m;
+    if (algo) *algo = p->algo;
+    return WINO_OK;
 }
 
 wino_plan *wino_conv_plan(int N, int C, int K, int H, int W, int m) {

@@ -62,6 +62,9 @@ hipError_t launch_frequency_gemm(const Geometry &g, const float *U, const float 
                                  hipStream_t s);
 hipError_t launch_output_transform(const Geometry &g, const float *M, float *y, hipStream_t s);
 
+// Sets the message wino_last_error() returns on the calling thread (printf format).
+void set_error(const char *fmt, ...);
+
 // Fused blocking the kernels are instantiated for, per m.
 bool fused_cfg_supported(int m, const FusedCfg &cfg);
 FusedCfg fused_cfg_default(const Geometry &g);

@@ -1,4 +1,5 @@
-"""Python binding of ``include/wino_conv.h`` (ctypes; argument marshalling only).
+"""Python binding of ``include/wino_conv.h`` and ``include/wino_tune.h`` (ctypes;
+argument marshalling only).
 
 The functions keep the C names.  Every computation runs in the HIP library
 ``libwino_conv.so``; if it is not built, the first call raises ``ImportError``
@@ -34,7 +35,20 @@ SIGNATURES = {
     "wino_conv_intermediate_dims": (_i, [_vp, _i, ctypes.POINTER(ctypes.c_longlong)]),
     "wino_conv_copy_intermediate": (_i, [_vp, _i, ctypes.POINTER(ctypes.c_float), ctypes.c_size_t]),
     "wino_last_error": (ctypes.c_char_p, []),
+    # wino_tune.h
+    "wino_conv_plan_tuned": (_vp, [_i, _i, _i, _i, _i, ctypes.c_uint, ctypes.POINTER(_i),
+                                   ctypes.POINTER(_i), ctypes.POINTER(ctypes.c_double)]),
+    "wino_conv_plan_params": (_i, [_vp, ctypes.POINTER(_i), ctypes.POINTER(_i)]),
+    "wino_wisdom_lookup": (_i, [ctypes.c_char_p, _i, _i, _i, _i, _i, _i, ctypes.c_uint,
+                                ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i)]),
+    "wino_wisdom_save": (_i, [ctypes.c_char_p]),
+    "wino_wisdom_load": (_i, [ctypes.c_char_p]),
+    "wino_wisdom_clear": (None, []),
+    "wino_wisdom_size": (_i, []),
 }
+
+WINO_TUNE_M2, WINO_TUNE_M4, WINO_TUNE_M6, WINO_TUNE_THREE_STAGE = 1 << 2, 1 << 4, 1 << 6, 1 << 8
+WINO_TUNE_ALL_M = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M6
 
 
 WINO_SCHED_AUTO, WINO_SCHED_SHARED, WINO_SCHED_PER_WAVE = 0, 1, 2
@@ -173,14 +187,65 @@ def wino_conv_copy_intermediate(plan, which):
     return out
 
 
+def wino_conv_plan_tuned(N, C, K, H, W, candidates=WINO_TUNE_ALL_M):
+    """(plan handle, m, algo, microseconds per call) of the fastest candidate."""
+    m, algo, us = ctypes.c_int(), ctypes.c_int(), ctypes.c_double()
+    p = lib().wino_conv_plan_tuned(N, C, K, H, W, candidates, ctypes.byref(m), ctypes.byref(algo),
+                                   ctypes.byref(us))
+    if not p:
+        raise WinoError(WINO_EINVAL, wino_last_error())
+    return p, m.value, algo.value, us.value
+
+
+def wino_conv_plan_params(plan):
+    """(m, algo) of a plan."""
+    m, algo = ctypes.c_int(), ctypes.c_int()
+    _check(lib().wino_conv_plan_params(plan, ctypes.byref(m), ctypes.byref(algo)))
+    return m.value, algo.value
+
+
+def wino_wisdom_lookup(arch, cus, N, C, K, H, W, candidates):
+    """(m, algo) of a wisdom entry, or None."""
+    found, m, algo = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check(lib().wino_wisdom_lookup(arch.encode(), cus, N, C, K, H, W, candidates,
+                                    ctypes.byref(found), ctypes.byref(m), ctypes.byref(algo)))
+    return (m.value, algo.value) if found.value else None
+
+
+def wino_wisdom_save(path):
+    return _check(lib().wino_wisdom_save(os.fsencode(path)))
+
+
+def wino_wisdom_load(path):
+    return _check(lib().wino_wisdom_load(os.fsencode(path)))
+
+
+def wino_wisdom_clear():
+    lib().wino_wisdom_clear()
+
+
+def wino_wisdom_size():
+    return int(lib().wino_wisdom_size())
+
+
 class Plan:
     """Owning wrapper of a plan handle (``with Plan(...) as p: p.run(x, w, y)``)."""
 
-    def __init__(self, N, C, K, H, W, m, algo="fused", tuning=None):
+    def __init__(self, N, C, K, H, W, m, algo="fused", tuning=None, _handle=None):
         self.shape = (N, C, K, H, W)
         self.m = m
         self.algo = algo
-        self.handle = wino_conv_plan_ex(N, C, K, H, W, m, algo, tuning)
+        self.handle = _handle if _handle is not None else wino_conv_plan_ex(N, C, K, H, W, m, algo,
+                                                                           tuning)
+
+    @classmethod
+    def tuned(cls, N, C, K, H, W, candidates=WINO_TUNE_ALL_M):
+        """The fastest plan among the candidates (timed now, or from the wisdom table);
+        its m, algorithm and measured call time are attributes."""
+        h, m, algo, us = wino_conv_plan_tuned(N, C, K, H, W, candidates)
+        p = cls(N, C, K, H, W, m, "fused" if algo == WINO_ALGO_FUSED else "three_stage", _handle=h)
+        p.call_us = us
+        return p
 
     def run(self, x, w, y, stream=None):
         wino_conv_run(self.handle, x, w, y, stream)

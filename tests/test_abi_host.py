@@ -1,8 +1,9 @@
-"""The C-ABI library loads and exports every symbol of include/wino_conv.h, and its
-host-side argument checks fail cleanly.  No GPU is touched: every case here is
-rejected before any HIP call is made."""
+"""The C-ABI library loads and exports every symbol of include/*.h, and its
+host-side argument checks fail cleanly; the wisdom table's file format round-trips.
+No GPU is touched: every case here is rejected before any HIP call is made."""
 
 import ctypes
+import glob
 import os
 import re
 
@@ -12,13 +13,15 @@ import paper_1912_02165_amd as wc
 from paper_1912_02165_amd import wino
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "wino_conv.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(wino_\w+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names.update(re.findall(r"\b(wino_\w+)\s*\(", text))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -104,3 +107,87 @@ def test_null_plan_calls(lib):
 def test_python_errors_raise(lib):
     with pytest.raises(wc.WinoError):
         wc.wino_conv_plan(1, 4, 4, 8, 8, 3)
+
+
+# ---- wisdom table (include/wino_tune.h), host only --------------------------
+
+WISDOM = """# winograd wisdom: arch cus N C K H W candidates m algo microseconds
+gfx950 256 32 64 64 224 224 0x54 4 0 417.900
+gfx950 256 64 512 512 14 14 0x154 6 1 12.500
+"""
+
+
+def test_wisdom_roundtrip(lib, tmp_path):
+    wc.wino_wisdom_clear()
+    assert wc.wino_wisdom_size() == 0
+    src = tmp_path / "in.txt"
+    src.write_text(WISDOM)
+    wc.wino_wisdom_load(str(src))
+    assert wc.wino_wisdom_size() == 2
+    assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (4, 0)
+    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1)
+    # every key field matters
+    assert wc.wino_wisdom_lookup("gfx942", 256, 32, 64, 64, 224, 224, 0x54) is None
+    assert wc.wino_wisdom_lookup("gfx950", 304, 32, 64, 64, 224, 224, 0x54) is None
+    assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x14) is None
+    out = tmp_path / "out.txt"
+    wc.wino_wisdom_save(str(out))
+    wc.wino_wisdom_clear()
+    wc.wino_wisdom_load(str(out))
+    assert wc.wino_wisdom_size() == 2
+    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1)
+    lines = [l for l in out.read_text().splitlines() if not l.startswith("#")]
+    assert sorted(lines) == sorted(l for l in WISDOM.splitlines() if not l.startswith("#"))
+    # a later entry with the same key replaces the earlier one
+    upd = tmp_path / "upd.txt"
+    upd.write_text("gfx950 256 32 64 64 224 224 0x54 2 0 500\n")
+    wc.wino_wisdom_load(str(upd))
+    assert wc.wino_wisdom_size() == 2
+    assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (2, 0)
+    wc.wino_wisdom_clear()
+
+
+@pytest.mark.parametrize("line", [
+    "gfx950 256 32 64 64 224 224 0x54 4 0",             # missing field
+    "gfx950 256 32 64 64 224 224 0x54 4 0 1.0 extra",   # extra field
+    "gfx950 256 32 64 64 224 224 0x54 3 0 1.0",         # m not a tile size
+    "gfx950 256 32 64 64 224 224 0x14 6 0 1.0",         # m not among the candidates
+    "gfx950 256 32 64 64 224 224 0x54 4 1 1.0",         # three-stage not a candidate
+    "gfx950 256 32 64 64 224 224 0x2 2 0 1.0",          # mask without a tile-size bit
+    "gfx950 256 32 0 64 224 224 0x54 4 0 1.0",          # size < 1
+    "gfx950 256 32 64 64 224 224 0x54 4 0 -1",          # negative time
+])
+def test_wisdom_rejects_malformed_and_keeps_table(lib, tmp_path, line):
+    wc.wino_wisdom_clear()
+    good = tmp_path / "good.txt"
+    good.write_text(WISDOM)
+    wc.wino_wisdom_load(str(good))
+    bad = tmp_path / "bad.txt"
+    bad.write_text("gfx950 256 1 1 1 1 1 0x4 2 0 1.0\n" + line + "\n")
+    with pytest.raises(wc.WinoError, match=r"bad.txt:2: malformed"):
+        wc.wino_wisdom_load(str(bad))
+    assert wc.wino_wisdom_size() == 2          # nothing of the bad file was merged
+    assert wc.wino_wisdom_lookup("gfx950", 256, 1, 1, 1, 1, 1, 0x4) is None
+    wc.wino_wisdom_clear()
+
+
+def test_wisdom_file_errors(lib, tmp_path):
+    with pytest.raises(wc.WinoError, match="cannot read"):
+        wc.wino_wisdom_load(str(tmp_path / "missing.txt"))
+    with pytest.raises(wc.WinoError, match="cannot write"):
+        wc.wino_wisdom_save(str(tmp_path / "no_such_dir" / "w.txt"))
+
+
+@pytest.mark.parametrize("mask", [0, wc.WINO_TUNE_THREE_STAGE, 1 << 3, wc.WINO_TUNE_M4 | (1 << 9)])
+def test_plan_tuned_bad_mask(lib, mask):
+    assert not lib.wino_conv_plan_tuned(1, 4, 4, 8, 8, mask, None, None, None)
+    assert "candidate mask" in wc.wino_last_error()
+
+
+def test_plan_tuned_bad_sizes(lib):
+    assert not lib.wino_conv_plan_tuned(1, 0, 4, 8, 8, wc.WINO_TUNE_ALL_M, None, None, None)
+    assert "sizes must be >= 1" in wc.wino_last_error()
+
+
+def test_plan_params_null(lib):
+    assert lib.wino_conv_plan_params(None, None, None) == wino.WINO_EINVAL

@@ -250,3 +250,45 @@ def test_unaligned_input_pointer(m):
         p.run(xd, torch.from_numpy(w).cuda(), y)
         torch.cuda.synchronize()
     assert_close(y.cpu().numpy(), direct_conv(x, w), m, f"unaligned x F({m})")
+
+
+# ---- tuned plans (include/wino_tune.h) --------------------------------------
+
+def _device_key():
+    prop = torch.cuda.get_device_properties(0)
+    return prop.gcnArchName.split(":")[0], prop.multi_processor_count
+
+
+@pytest.mark.parametrize("mask", [wc.WINO_TUNE_ALL_M | wc.WINO_TUNE_THREE_STAGE, wc.WINO_TUNE_M4,
+                                  wc.WINO_TUNE_M2 | wc.WINO_TUNE_M6])
+def test_plan_tuned(mask, tmp_path):
+    """The tuned plan is one of the candidates, matches the oracle at its m, and is
+    remembered: the second request, and one after a save / clear / load of the
+    wisdom table, return the same choice without timing again."""
+    N, C, K, H, W = 2, 37, 45, 29, 35
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=95)
+    print(f"\n[gpu] tuned plan mask={mask:#x}", flush=True)
+    wc.wino_wisdom_clear()
+    p = wc.Plan.tuned(N, C, K, H, W, mask)
+    assert mask & (1 << p.m)
+    assert p.algo == "fused" or mask & wc.WINO_TUNE_THREE_STAGE
+    assert wc.wino_conv_plan_params(p.handle) == (p.m, wc.ALGOS[p.algo])
+    assert p.call_us > 0
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    y = torch.full((N, K, H, W), float("nan"), device="cuda")
+    p.run(xd, wd, y)
+    torch.cuda.synchronize()
+    assert_close(y.cpu().numpy(), direct_conv(x, w), p.m, f"tuned F({p.m}) {p.algo}")
+    arch, cus = _device_key()
+    assert wc.wino_wisdom_lookup(arch, cus, N, C, K, H, W, mask) == (p.m, wc.ALGOS[p.algo])
+    p2 = wc.Plan.tuned(N, C, K, H, W, mask)
+    assert (p2.m, p2.algo, p2.call_us) == (p.m, p.algo, p.call_us)
+    f = tmp_path / "wisdom.txt"
+    wc.wino_wisdom_save(str(f))
+    wc.wino_wisdom_clear()
+    wc.wino_wisdom_load(str(f))
+    p3 = wc.Plan.tuned(N, C, K, H, W, mask)
+    assert (p3.m, p3.algo) == (p.m, p.algo) and abs(p3.call_us - p.call_us) < 1e-3
+    for q in (p, p2, p3):
+        q.close()
+    wc.wino_wisdom_clear()
