@@ -32,6 +32,10 @@ The divisor of L_j is moved from Interp^T to row j of Eval_g, so
 Point sets (in frequency order; infinity is always last):
     F(2,3): 0, 1, -1
     F(4,3): 0, 1, -1, 2, -2
+    F(5,3): 1, -1, 2, -2, 1/2, -1/2     (the paper's T = 7 tile, Sec. 6; the paper
+                                         gives no points: six finite points in +-p
+                                         pairs, without 0, so that every point
+                                         but infinity has its mirror)
     F(6,3): 0, 1, -1, 2, -2, 1/2, -1/2
 """
 
@@ -42,6 +46,7 @@ R = 3  # kernel edge: the paper's K for 3x3 kernels
 _POINTS = {
     2: (Fraction(0), Fraction(1), Fraction(-1)),
     4: (Fraction(0), Fraction(1), Fraction(-1), Fraction(2), Fraction(-2)),
+    5: (Fraction(1), Fraction(-1), Fraction(2), Fraction(-2), Fraction(1, 2), Fraction(-1, 2)),
     6: (Fraction(0), Fraction(1), Fraction(-1), Fraction(2), Fraction(-2),
         Fraction(1, 2), Fraction(-1, 2)),
 }

@@ -3,13 +3,15 @@
 Tolerances (relative L2 error over the compared outputs, and the largest
 element error normalised by the largest reference magnitude):
     F(2x2,3x3): rel_l2 <= 1e-5;  F(4x4,3x3), F(6x6,3x3): rel_l2 <= 1e-4;
+    F(5x5,3x3) (not among the stated tolerances; its tile lies between F(4) and
+    F(6), so it takes theirs): rel_l2 <= 1e-4;
     all: max|y - y_ref| / max|y_ref| <= 1e-3.
 The reference is the fp64 oracle; the GPU computes in fp32.
 """
 
 import numpy as np
 
-REL_L2 = {2: 1e-5, 4: 1e-4, 6: 1e-4}
+REL_L2 = {2: 1e-5, 4: 1e-4, 5: 1e-4, 6: 1e-4}
 MAX_ERR = 1e-3
 
 

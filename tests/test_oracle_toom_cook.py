@@ -111,16 +111,24 @@ def test_f2_tables_by_hand():
 
 
 def test_points_pair_structure():
-    """Points come in +-p pairs after 0, so B^T rows of a pair agree on even
-    coefficients and are negated on odd ones (a property the GPU code may use)."""
+    """Points come in +-p pairs (after 0 when 0 is a point: even T), so the B^T rows
+    of a pair are the same polynomial at x and -x (coefficient i times (-1)^i, and
+    negated once more when 0 is not a point: the row's degree is then odd), and A^T
+    columns of a pair differ by (-1)^i (properties the GPU code may use)."""
     for m in MS:
         p = toom_cook.points(m)
-        _, _, BT = toom_cook.matrices(m)
-        assert p[0] == 0
-        for j in range(1, len(p), 2):
+        AT, _, BT = toom_cook.matrices(m)
+        assert len(p) == m + 1
+        j0 = 1 if p[0] == 0 else 0
+        assert (j0 == 1) == (m % 2 == 0)
+        assert 0 not in p[j0:]
+        for j in range(j0, len(p), 2):
             assert p[j + 1] == -p[j]
+            for i in range(m):
+                assert AT[i][j + 1] == (AT[i][j] if i % 2 == 0 else -AT[i][j])
+            sgn = 1 if j0 == 1 else -1
             for i, (a, b) in enumerate(zip(BT[j], BT[j + 1])):
-                assert b == (a if i % 2 == 0 else -a)
+                assert b == sgn * (a if i % 2 == 0 else -a)
 
 
 def test_unsupported_m():
