@@ -9,7 +9,8 @@
  * with x read as zero outside the image (implicit padding), stride 1.  It is
  * computed as the Winograd F(m x m, 3 x 3) transformed convolution of Eq. 3,
  * y = A^T [ sum_c (G w G^T) (.) (B^T d B) ] A over overlap-add tiles of edge
- * T = m + 2 (Sec. 2.1), for m in {2, 4, 6}.
+ * T = m + 2 (Sec. 2.1), for m in {2, 4, 5, 6} (m = 5, T = 7, is the tile of the
+ * paper's experiments, Sec. 6).
  *
  * Layouts: x is N x C x H x W, w is K x C x 3 x 3, y is N x K x H x W, all dense
  * row-major fp32.  x, w and y are device pointers on the plan's device.
@@ -98,7 +99,7 @@ typedef struct {
  * transformed kernels (T^2 * C * K floats rounded up to the blocking) and, when
  * the last round of work items is split across compute units, their partial
  * outputs and arrival counters (zeroed here; every call leaves them zero).
- * Returns NULL (see wino_last_error) if a size is < 1, m is not 2, 4 or 6, a
+ * Returns NULL (see wino_last_error) if a size is < 1, m is not 2, 4, 5 or 6, a
  * size overflows the 32-bit offsets the kernels use (each of x and y must be
  * below 2^31 bytes), or the allocation fails. */
 wino_plan *wino_conv_plan(int N, int C, int K, int H, int W, int m);
@@ -141,10 +142,11 @@ int wino_conv_info(const wino_plan *p, long long *n_tiles, double *direct_flops,
 
 /* Logical layout of an intermediate buffer as up to 4 dims (outermost first,
  * unused trailing dims are 1), for tests that read it back:
- *   WINO_BUF_WEIGHTS: [Kb][Cs][T^2/4][64][4]: element (f, c, k) of G w[k,c] G^T
- *                     sits at kb = k/16, cs = c/4, block f/4, lane (c%4)*16 + k%16,
- *                     slot f%4 (the matrix-core operand order).  Dims returned:
- *                     {Kb, Cs, T^2, 64} with f in the third dim as described.
+ *   WINO_BUF_WEIGHTS: [Kb][Cs][Q][64][4], Q = ceil(T^2/4): element (f, c, k) of
+ *                     G w[k,c] G^T sits at kb = k/16, cs = c/4, block f/4, lane
+ *                     (c%4)*16 + k%16, slot f%4 (the matrix-core operand order);
+ *                     slots past f = T^2 - 1 (F(5)) hold zeros.  Dims returned:
+ *                     {Kb, Cs, 4*Q, 64} with f in the third dim as described.
  *   WINO_BUF_INPUT:   [T^2][Cp][tiles_p]  (three-stage plans only)
  *   WINO_BUF_PRODUCT: [T^2][Kp][tiles_p]  (three-stage plans only)
  * Frequency f = i*T + j for transform row i, column j; tile t = (n*TH + ty)*TW + tx. */

@@ -4,9 +4,9 @@
  * Sec. 6 runs one fixed configuration on every layer and notes that tuning the
  * parameters for each particular layer can only improve the results; Sec. 7
  * says that tuning is done once and stored in a wisdom file.  Here the tuned
- * parameter is the tile size m of F(m x m, 3 x 3) (the paper's T = m + 2; the
- * number of tiles per task is fixed by the matrix-core blocking) and, optionally,
- * the algorithm (fused or three-stage).  A tuning result is remembered per
+ * parameter is the tile size m of F(m x m, 3 x 3), m in {2, 4, 5, 6} (the
+ * paper's T = m + 2; the number of tiles per task is fixed by the matrix-core
+ * blocking) and, optionally, the algorithm (fused or three-stage).  A tuning result is remembered per
  * (GPU architecture, compute units, N, C, K, H, W, candidate set) in a
  * process-wide wisdom table that can be written to and read from a text file.
  *
@@ -33,6 +33,7 @@ extern "C" {
 enum {
     WINO_TUNE_M2 = 1 << 2,
     WINO_TUNE_M4 = 1 << 4,
+    WINO_TUNE_M5 = 1 << 5,
     WINO_TUNE_M6 = 1 << 6,
     WINO_TUNE_THREE_STAGE = 1 << 8
 };

@@ -59,8 +59,8 @@ int make_geometry(int N, int C, int K, int H, int W, int m, Geometry *g) {
         set_err("sizes must be >= 1 (N=%d C=%d K=%d H=%d W=%d)", N, C, K, H, W);
         return WINO_EINVAL;
     }
-    if (m != 2 && m != 4 && m != 6) {
-        set_err("m=%d: only F(2x2,3x3), F(4x4,3x3) and F(6x6,3x3) are supported", m);
+    if (m != 2 && m != 4 && m != 5 && m != 6) {
+        set_err("m=%d: only F(2x2,3x3), F(4x4,3x3), F(5x5,3x3) and F(6x6,3x3) are supported", m);
         return WINO_EINVAL;
     }
     const long long T = m + 2, TH = (H + m - 1) / m, TW = (W + m - 1) / m;
@@ -227,7 +227,8 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
                 cfg.schedule, cfg.nkb, cfg.waves, cfg.tb, m);
         return nullptr;
     }
-    const size_t wt_bytes = (size_t)g.Kb_alloc * 16 * g.Cs * 4 * g.T2 * sizeof(float);
+    // frequencies in float4 groups, the last one padded when T^2 is odd (F(5))
+    const size_t wt_bytes = (size_t)g.Kb_alloc * 16 * g.Cs * 4 * ((g.T2 + 3) / 4 * 4) * sizeof(float);
     size_t U_bytes = 0, M_bytes = 0;
     if (algo == WINO_ALGO_THREE_STAGE) {
         U_bytes = (size_t)g.T2 * g.Cs * 4 * g.tiles_p * sizeof(float);
@@ -409,7 +410,7 @@ int wino_conv_intermediate_dims(const wino_plan *p, int which, long long dims[4]
     const Geometry &g = p->g;
     switch (which) {
         case WINO_BUF_WEIGHTS:
-            dims[0] = g.Kb_alloc; dims[1] = g.Cs; dims[2] = g.T2; dims[3] = 64;
+            dims[0] = g.Kb_alloc; dims[1] = g.Cs; dims[2] = (g.T2 + 3) / 4 * 4; dims[3] = 64;
             return WINO_OK;
         case WINO_BUF_INPUT:
             if (!p->U) break;

@@ -83,12 +83,17 @@ struct TileLoader {
     }
 };
 
+// Frequencies are grouped in float4s (four consecutive f) for the matrix-core
+// operands; T^2 = 49 (F(5)) ends with a partial group padded with zeros.
+template <int M>
+constexpr int freq_quads() { return ((M + 2) * (M + 2) + 3) / 4; }
+
 // ---------------------------------------------------------------------------
 // Kernel transform (Sec. 3, step 2: right-hand matrices transformed ahead of
 // time).  Thread (kb, cs, lane) transforms kernel (k, c) with k = 16 kb + lane%16,
 // c = 4 cs + lane/16 and stores the T^2 values in matrix-core operand order:
-// wt[((kb * Cs + cs) * T^2/4 + f/4) * 64 + lane][f % 4].  Channels >= C and
-// output channels >= K are stored as zeros.
+// wt[((kb * Cs + cs) * Q + f/4) * 64 + lane][f % 4], Q = ceil(T^2/4).  Channels
+// >= C, output channels >= K and frequencies >= T^2 are stored as zeros.
 template <int M>
 __global__ void __launch_bounds__(256) weight_transform_kernel(const float *__restrict__ w,
                                                                floatx4 *__restrict__ wt, Geometry g) {
@@ -107,11 +112,14 @@ __global__ void __launch_bounds__(256) weight_transform_kernel(const float *__re
     const float *src = w + ((long long)(ok ? k : 0) * g.C + (ok ? c : 0)) * 9;
 #pragma unroll
     for (int i = 0; i < 9; ++i) gk[i] = ok ? src[i] : 0.0f;
-    float t[T2];
+    constexpr int Q = freq_quads<M>();
+    float t[4 * Q];
     kernel_tile_transform<M>(gk, t);
-    floatx4 *dst = wt + grp * (T2 / 4) * 64 + lane;
 #pragma unroll
-    for (int f4 = 0; f4 < T2 / 4; ++f4) {
+    for (int f = T2; f < 4 * Q; ++f) t[f] = 0.0f;
+    floatx4 *dst = wt + grp * Q * 64 + lane;
+#pragma unroll
+    for (int f4 = 0; f4 < Q; ++f4) {
         floatx4 v = {t[4 * f4], t[4 * f4 + 1], t[4 * f4 + 2], t[4 * f4 + 3]};
         dst[f4 * 64] = v;
     }
@@ -138,6 +146,8 @@ __device__ void buffer_store_f32x4(floatx4 v, int32x4 rsrc, unsigned voffset, un
     __asm("llvm.amdgcn.raw.buffer.store.v4f32");
 __device__ void buffer_store_f32x2(floatx2 v, int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
     __asm("llvm.amdgcn.raw.buffer.store.v2f32");
+__device__ void buffer_store_f32(float v, int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.store.f32");
 // Cache-policy bit of a buffer access that makes it coherent across the device
 // (the coherence that device-scope atomic loads and stores use).
 constexpr int kDeviceCoherent = 1 << 4;
@@ -325,8 +335,8 @@ struct RowTile {
     __device__ __forceinline__ void issue(int32x4 r, float *d) const {
 #pragma unroll
         for (int a = 0; a < T; ++a) {
-            // Own columns with one vector load for m = 2, 4 and two (4 + 2) for
-            // m = 6 (rows 8-byte aligned).  roff is below 2^31 or exactly 2^31 and
+            // Own columns with one vector load for m = 2, 4 and two for m = 6 (4 + 2,
+            // rows 8-byte aligned) and m = 5 (4 + 1).  roff is below 2^31 or exactly 2^31 and
             // own + 4*M is below 2^31, so the offsets never wrap.
             const unsigned base = roff[a] + own;
             if constexpr (M == 4) {
@@ -340,8 +350,13 @@ struct RowTile {
                 for (int j = 0; j < 4; ++j) d[a * T + 1 + j] = q[j];
                 d[a * T + 5] = q2[0];
                 d[a * T + 6] = q2[1];
+            } else if constexpr (M == 5) {  // rows 4-byte aligned
+                const floatx4 q = buffer_load_f32x4(r, base, 0, 0);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) d[a * T + 1 + j] = q[j];
+                d[a * T + 5] = buffer_load_f32(r, base + 16u, 0, 0);
             } else {
-                static_assert(M == 2, "m = 2, 4 or 6");
+                static_assert(M == 2, "m = 2, 4, 5 or 6");
                 const floatx2 q = buffer_load_f32x2(r, base, 0, 0);
                 d[a * T + 1] = q[0];
                 d[a * T + 2] = q[1];
@@ -646,6 +661,9 @@ __device__ __forceinline__ void store_rows_buf(int32x4 yrs, unsigned voff, unsig
         const unsigned so = soff + (unsigned)i * rowb;
         if constexpr (M == 4) {
             buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, 0);
+        } else if constexpr (M == 5) {  // 4-byte aligned vector store + one float
+            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, 0);
+            buffer_store_f32(yy[i * M + 4], yrs, voff + 16u, so, 0);
         } else {
 #pragma unroll
             for (int jj = 0; jj < M; jj += 2)
@@ -655,7 +673,8 @@ __device__ __forceinline__ void store_rows_buf(int32x4 yrs, unsigned voff, unsig
 }
 
 // Store one m x m output tile of plane yp (clipped to H x W).  vec: rows may be
-// written with m-float vector stores (16-byte aligned for m = 4, 8-byte for m = 2, 6).
+// written with m-float vector stores (16-byte aligned for m = 4, 8-byte for m = 2, 6;
+// m = 5 always stores element by element here).
 template <int M>
 __device__ __forceinline__ void store_tile(float *__restrict__ yp, const float *yy, int h0, int w0,
                                            const Geometry &g, bool vec) {
@@ -664,11 +683,11 @@ __device__ __forceinline__ void store_tile(float *__restrict__ yp, const float *
         const int h = h0 + i;
         if (h >= g.H) break;
         float *row = yp + (long long)h * g.W + w0;
-        if (vec && w0 + M <= g.W) {
+        if (M != 5 && vec && w0 + M <= g.W) {
             if constexpr (M == 4) {
                 *reinterpret_cast<floatx4 *>(row) =
                     floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]};
-            } else {
+            } else if constexpr (M != 5) {
                 #pragma unroll
                 for (int jj = 0; jj < M; jj += 2)
                     *reinterpret_cast<floatx2 *>(row + jj) = floatx2{yy[i * M + jj], yy[i * M + jj + 1]};
@@ -702,18 +721,31 @@ __device__ __forceinline__ void store_tile(float *__restrict__ yp, const float *
 // overlap the matrix cores.  LDS holds two stage buffers with one barrier per
 // stage; the layout of a buffer is that of fused_shared_kernel.
 
-// Transform-domain rows owned by frequency group G of FS (bit i = row i).
+// Transform-domain rows owned by frequency group G of FS (bit i = row i).  Each
+// group is closed under the (+p, -p) row pairs and covers whole float4s of
+// frequencies: F(6) (T = 8, a row is two float4s): rows {0,1,2,7} and {3,4,5,6};
+// F(5) (T = 7): rows {0..3} = frequencies 0..27 = float4s 0..6 and rows {4,5,6} =
+// float4s 7..12 (the last padded).
 template <int M, int FS, int G>
 constexpr unsigned group_rows() {
     if constexpr (FS == 1) return (1u << (M + 2)) - 1u;
-    else return G == 0 ? 0x87u : 0x78u;  // F(6): rows {0,1,2,7} and {3,4,5,6}
+    else if constexpr (M == 5) return G == 0 ? 0x0fu : 0x70u;
+    else return G == 0 ? 0x87u : 0x78u;
 }
 
-// Global float4 frequency indices of the group's float4s, as a compile-time
-// table (T = 8: a transform-domain row is two float4s).
+// Global float4 frequency indices of the group's float4s (those holding a
+// frequency of the group's rows), as a compile-time table.
 template <int M, int FS, int G>
 struct GroupF4 {
-    static constexpr int N = (M + 2) * (M + 2) / 4 / FS;
+    static constexpr int T = M + 2;
+    static constexpr int Q = freq_quads<M>();
+    static constexpr int count() {
+        int n = 0;
+        for (int q = 0; q < Q; ++q)
+            if ((group_rows<M, FS, G>() >> ((4 * q) / T)) & 1u) ++n;
+        return n;
+    }
+    static constexpr int N = count();
     int f4[N];
     // accumulator index (4 * position of the float4 + offset) of frequency f
     constexpr int index(int f) const {
@@ -722,17 +754,20 @@ struct GroupF4 {
         return -1;
     }
     constexpr GroupF4() : f4{} {
-        constexpr unsigned rows = group_rows<M, FS, G>();
-        if (FS == 1) {
-            for (int i = 0; i < N; ++i) f4[i] = i;
-        } else {
-            int n = 0;
-            for (int i = 0; i < M + 2; ++i)
-                if ((rows >> i) & 1u) {
-                    f4[n++] = 2 * i;
-                    f4[n++] = 2 * i + 1;
-                }
+        int n = 0;
+        for (int q = 0; q < Q; ++q)
+            if ((group_rows<M, FS, G>() >> ((4 * q) / T)) & 1u) f4[n++] = q;
+    }
+    // every float4 lies within the group's rows (the group splits on float4 bounds)
+    static constexpr bool whole() {
+        for (int q = 0; q < Q; ++q) {
+            const unsigned r0 = (group_rows<M, FS, G>() >> ((4 * q) / T)) & 1u;
+            for (int e = 1; e < 4; ++e) {
+                const int f = 4 * q + e;
+                if (f < T * T && ((group_rows<M, FS, G>() >> (f / T)) & 1u) != r0) return false;
+            }
         }
+        return true;
     }
 };
 
@@ -907,15 +942,17 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
                                            const floatx4 *__restrict__ wt, float *__restrict__ y,
                                            const Geometry &g, const WsSeq &sq, const WsSplit &sp,
                                            int n_inner, int kbl, int lane, int vec) {
-    constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
+    constexpr int T = M + 2, F4 = freq_quads<M>();
     constexpr int R = 16 * TB, CC = 256 / R, SS = CC / 4, BUF = F4 * CC * R;
     constexpr int NSLOT = ws_slots<M>();
-    constexpr int NF4 = F4 / FS;
+    constexpr GroupF4<M, FS, G> gm{};
+    constexpr int NF4 = gm.N;  // float4s of frequencies this wave multiplies
     constexpr int KBW = 4 / FS;
     constexpr int MM = M * M;
+    constexpr int MMP = (MM + 3) / 4 * 4;  // output tile padded to whole float4s
     constexpr unsigned ROWS = group_rows<M, FS, G>();
-    static_assert(FS == 1 || T == 8, "frequency split is built for F(6) only");
-    constexpr GroupF4<M, FS, G> gm{};
+    static_assert(FS == 1 || T >= 7, "frequency split is built for F(5) and F(6)");
+    static_assert(gm.whole() && rows_pair_closed<M, ROWS>(), "groups split on float4 and pair bounds");
     const long long HW = (long long)g.H * g.W;
     const int32x4 yrs = make_rsrc(y, (unsigned)((long long)g.N * g.K * HW * 4));
     const unsigned hwb = (unsigned)(HW * 4), rowb = (unsigned)g.W * 4u;
@@ -938,9 +975,8 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
     const unsigned vo = (unsigned)lane * 16u;
     // partial outputs of a contributor: [kbl][t][v][lane][element] floats, so a
     // lane's output tile is contiguous (16-byte accesses)
-    static_assert(MM % 4 == 0, "output tiles are whole float4s");
-    const unsigned vlane = (unsigned)lane * MM * 4u;
-    auto poff = [&](int t, int v) { return (unsigned)((((kbl * TB + t) * 4 + v) * 64) * MM) * 4u; };
+    const unsigned vlane = (unsigned)lane * MMP * 4u;
+    auto poff = [&](int t, int v) { return (unsigned)((((kbl * TB + t) * 4 + v) * 64) * MMP) * 4u; };
     auto wbase = [&](int it) { return (unsigned)((item_kgroup<KM>(it, n_inner) * KBW + kbl) * g.Cs) * SB; };
     auto wload = [&](unsigned soff, int lf) { return buffer_load_f32x4(wrs, vo, soff + gm.f4[lf] * 1024u, 0); };
     const int last = g.Cs - 1;
@@ -1089,21 +1125,21 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
                 const TileIdx ti = decode_tile(g, tile0 + t * 16 + (lane & 15));
                 const bool whole = whole_of(ti);
                 for (int v = 0; v < 4; ++v) {
-                    float yy[MM];
+                    float yy[MMP];
 #pragma unroll
-                    for (int e = 0; e < MM; ++e) yy[e] = 0.0f;
+                    for (int e = 0; e < MMP; ++e) yy[e] = 0.0f;
                     // CH contributors' partials are loaded before any is added (one
                     // memory round trip per CH contributors); the additions keep
                     // contributor order
-                    constexpr int CH = MM >= 36 ? 2 : 4;
+                    constexpr int CH = MMP >= 28 ? 2 : 4;
                     for (int jc0 = 0; jc0 < ncontrib_; jc0 += CH) {
-                        floatx4 pv[CH][MM / 4];
+                        floatx4 pv[CH][MMP / 4];
 #pragma unroll
                         for (int c = 0; c < CH; ++c) {
                             const int jc = jc0 + c < ncontrib_ ? jc0 + c : ncontrib_ - 1;
                             const unsigned o = (unsigned)(jc * sp.part_floats) * 4u + poff(t, v);
 #pragma unroll
-                            for (int e = 0; e < MM / 4; ++e) pv[c][e] = buffer_load_f32x4(all, vlane, o + e * 16u, kDeviceCoherent);
+                            for (int e = 0; e < MMP / 4; ++e) pv[c][e] = buffer_load_f32x4(all, vlane, o + e * 16u, kDeviceCoherent);
                         }
 #pragma unroll
                         for (int c = 0; c < CH; ++c) {
@@ -1143,9 +1179,10 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
                 store(ti, k_out, v, yy, whole_of(ti));
             } else {
 #pragma unroll
-                for (int e = 0; e < MM; e += 4)
-                    buffer_store_f32x4(floatx4{yy[e], yy[e + 1], yy[e + 2], yy[e + 3]}, mine, vlane,
-                                       poff(t, v) + e * 4u, kDeviceCoherent);
+                for (int e = 0; e < MMP; e += 4)
+                    buffer_store_f32x4(floatx4{yy[e], e + 1 < MM ? yy[e + 1] : 0.0f, e + 2 < MM ? yy[e + 2] : 0.0f,
+                                               e + 3 < MM ? yy[e + 3] : 0.0f},
+                                       mine, vlane, poff(t, v) + e * 4u, kDeviceCoherent);
             }
         });
         if (partial) {
@@ -1190,7 +1227,7 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
                                                        const floatx4 *__restrict__ wt,
                                                        float *__restrict__ y, Geometry g, int vec,
                                                        int n_inner, int n_items, WsSplit sp) {
-    constexpr int T = M + 2, T2 = T * T, F4 = T2 / 4;
+    constexpr int T = M + 2, T2 = T * T, F4 = freq_quads<M>();
     constexpr int R = 16 * TB;
     constexpr int CC = 256 / R;
     constexpr int BUF = F4 * CC * R;
@@ -1592,7 +1629,7 @@ __global__ void __launch_bounds__(256) frequency_gemm_kernel(const float *__rest
     for (int cs = 0; cs < g.Cs; ++cs) {
         float a[KBW], b[TBW];
 #pragma unroll
-        for (int i = 0; i < KBW; ++i) a[i] = wb[((long long)(kb0 + i) * g.Cs + cs) * T2 * 64];
+        for (int i = 0; i < KBW; ++i) a[i] = wb[((long long)(kb0 + i) * g.Cs + cs) * (4 * freq_quads<M>()) * 64];
 #pragma unroll
         for (int j = 0; j < TBW; ++j) b[j] = ub[(long long)cs * 4 * g.tiles_p + j * 16];
 #pragma unroll
@@ -1648,6 +1685,7 @@ __global__ void __launch_bounds__(256) output_transform_kernel(const float *__re
     switch (m) {                          \
         case 2: { constexpr int MM = 2; CALL; } break; \
         case 4: { constexpr int MM = 4; CALL; } break; \
+        case 5: { constexpr int MM = 5; CALL; } break; \
         case 6: { constexpr int MM = 6; CALL; } break; \
         default: return hipErrorInvalidValue; \
     }
@@ -1661,8 +1699,9 @@ hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt,
 }
 
 bool fused_cfg_supported(int m, const FusedCfg &cfg) {
-    if (m != 2 && m != 4 && m != 6) return false;
+    if (m != 2 && m != 4 && m != 5 && m != 6) return false;
     if (cfg.schedule == kSchedSpecialised) return true;
+    if (m == 5) return false;  // F(5) runs only the warp-specialised kernel
     if (cfg.schedule == kSchedPersistent) return m == 2;
     if (cfg.schedule == kSchedShared) return cfg.tb == 1 || (cfg.tb == 2 && m <= 4);
     if (cfg.schedule != kSchedPerWave) return false;
@@ -1701,7 +1740,7 @@ static SplitInfo ws_split_info(const Geometry &g, int num_cus) {
     const int cus = num_cus < 1 ? 1 : num_cus;
     si.nfull = si.n_items / cus;
     si.grid = si.n_items < cus ? si.n_items : cus;
-    si.part_floats = KBW * TB * 4 * M * M * 64;
+    si.part_floats = KBW * TB * 4 * ((M * M + 3) / 4 * 4) * 64;  // output tiles padded to float4s
     si.tail_first = si.n_items;  // every item whole unless split below
     si.n_tail = 0;
     si.tail_units = 0;
@@ -1733,6 +1772,7 @@ SplitInfo fused_split_info(const Geometry &g, const FusedCfg &cfg) {
     switch (g.m) {
         case 2: return ws_split_info<2, 2, 1>(g, cfg.num_cus);
         case 4: return ws_split_info<4, 1, 1>(g, cfg.num_cus);
+        case 5: return ws_split_info<5, 1, 2>(g, cfg.num_cus);
         default: return ws_split_info<6, 1, 2>(g, cfg.num_cus);
     }
 }
@@ -1752,7 +1792,8 @@ static void launch_ws_t(const Geometry &g, const float *x, const float *wt, floa
     sp.part_floats = si.part_floats;
     dim3 block(512), grid((unsigned)si.grid);
     // row-vector input loads need every row start aligned to the vector width
-    const unsigned vw = (M == 4) ? 16u : 8u;
+    // (m = 5: 4-byte aligned vector loads)
+    const unsigned vw = (M == 4) ? 16u : (M == 5) ? 4u : 8u;
     const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
     // Item order: when the transformed kernels outweigh the input (deep layers),
     // the tile groups of one output-channel group are numbered adjacently, so the
@@ -1817,7 +1858,10 @@ hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, 
                         float *y, const SplitBuffers &sb, hipStream_t s) {
     if (!fused_cfg_supported(g.m, cfg)) return hipErrorInvalidValue;
     const uintptr_t ya = reinterpret_cast<uintptr_t>(y);
-    const bool vec = (g.m == 4) ? (g.W % 4 == 0 && ya % 16 == 0) : (g.W % 2 == 0 && ya % 8 == 0);
+    // rows of whole tiles stored as vectors: 16-byte aligned for m = 4, 8-byte for m =
+    // 2, 6; m = 5 uses buffer stores that need only 4-byte alignment
+    const bool vec = (g.m == 5) ? true
+                     : (g.m == 4) ? (g.W % 4 == 0 && ya % 16 == 0) : (g.W % 2 == 0 && ya % 8 == 0);
     if (cfg.schedule == kSchedPersistent) {
         launch_1w_t<2, 4>(g, x, wt, y, vec, cfg.num_cus, s);
         return hipGetLastError();
@@ -1826,6 +1870,7 @@ hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, 
         switch (g.m) {
             case 2: launch_ws_t<2, 2, 1>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
             case 4: launch_ws_t<4, 1, 1>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
+            case 5: launch_ws_t<5, 1, 2>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
             default: launch_ws_t<6, 1, 2>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
         }
         return hipGetLastError();

@@ -10,13 +10,16 @@
 //   B^T[j][a] = coefficient of x^a in prod_{l!=j}(x - p_l)
 //               (infinity row: coefficients of prod_l (x - p_l)).
 // Points, in frequency order: F(2): 0, 1, -1; F(4): 0, +-1, +-2;
+// F(5): +-1, +-2, +-1/2 (no 0: T = 7 has an even number of finite points);
 // F(6): 0, +-1, +-2, +-1/2.
 //
-// Because the finite points are 0 followed by (+p, -p) pairs, the B^T rows of a
-// pair agree on even coefficients and differ in sign on odd ones, and the A^T
-// columns of a pair differ by (-1)^i.  The 1D transforms below use that to share
-// work between the two rows (even part +- odd part).  Every coefficient is a
-// compile-time constant: zero terms vanish, +-1 become adds and subtracts.
+// Because the finite points are (+p, -p) pairs (after 0 for even T), the B^T rows
+// of a pair are one polynomial at x and -x: they agree on even coefficients and
+// differ in sign on odd ones (and are negated once more for odd T, whose rows
+// have odd degree), and the A^T columns of a pair differ by (-1)^i.  The 1D
+// transforms below use that to share work between the two rows (even part +-
+// odd part).  Every coefficient is a compile-time constant: zero terms vanish,
+// +-1 become adds and subtracts.
 #pragma once
 
 namespace wino {
@@ -51,11 +54,19 @@ constexpr bool operator==(Q a, Q b) { return a.n == b.n && a.d == b.d; }
 constexpr float to_float(Q a) { return (float)((double)a.n / (double)a.d); }
 
 constexpr Q point(int m, int j) {
-    // 0, 1, -1, 2, -2, 1/2, -1/2 (the first m + 1 are used)
+    // 0, 1, -1, 2, -2, 1/2, -1/2: the first m + 1 for even m, without 0 for odd m
     constexpr long long num[7] = {0, 1, -1, 2, -2, 1, -1};
     constexpr long long den[7] = {1, 1, 1, 1, 1, 2, 2};
-    return (void)m, mkq(num[j], den[j]);
+    const int i = (m % 2 == 1) ? j + 1 : j;
+    return mkq(num[i], den[i]);
 }
+
+// First row (B^T) / column (A^T) of the (+p, -p) pairs: 1 when 0 is a point (even
+// T), else 0; and the extra sign between the B^T rows of a pair.
+template <int M>
+constexpr int pair0() { return (M % 2 == 0) ? 1 : 0; }
+template <int M>
+constexpr float pair_sign() { return (M % 2 == 0) ? 1.0f : -1.0f; }
 
 template <int M>
 struct Tables {
@@ -110,19 +121,21 @@ template <int M>
 constexpr bool pair_structure_holds() {
     constexpr Tables<M> tb{};
     constexpr int T = M + 2;
-    for (int j = 1; j + 1 < T - 1; j += 2) {
+    constexpr float sg = pair_sign<M>();
+    for (int j = pair0<M>(); j + 1 < T - 1; j += 2) {
         for (int a = 0; a < T; ++a) {
             float e = tb.bt[j][a], o = tb.bt[j + 1][a];
-            if (a % 2 == 0 ? (e != o) : (e != -o)) return false;
+            if (a % 2 == 0 ? (o != sg * e) : (o != -sg * e)) return false;
         }
         for (int i = 0; i < M; ++i) {
             float e = tb.at[i][j], o = tb.at[i][j + 1];
             if (i % 2 == 0 ? (e != o) : (e != -o)) return false;
         }
     }
-    return true;
+    return (T - 1 - pair0<M>()) % 2 == 0;  // every finite point but 0 is paired
 }
-static_assert(pair_structure_holds<2>() && pair_structure_holds<4>() && pair_structure_holds<6>(),
+static_assert(pair_structure_holds<2>() && pair_structure_holds<4>() && pair_structure_holds<5>() &&
+                  pair_structure_holds<6>(),
               "B^T rows / A^T columns of +-p points must pair up");
 
 // acc (op)= c * v with a compile-time coefficient; `first` starts the sum.
@@ -184,20 +197,20 @@ __device__ __forceinline__ void bt_1d(const float *in, float *out) {
     constexpr Tables<M> tb{};
     constexpr OddScale<M> os{};
     constexpr int T = M + 2;
-    // p = 0 and the point at infinity: plain rows
-    out[0] = dot_unit_first<T, SI, 0, 1>(tb.bt[0], in);
+    // p = 0 (even T) and the point at infinity: plain rows
+    if constexpr (pair0<M>() == 1) out[0] = dot_unit_first<T, SI, 0, 1>(tb.bt[0], in);
     out[(T - 1) * SO] = dot_unit_first<T, SI, 0, 1>(tb.bt[T - 1], in);
 #pragma unroll
-    for (int j = 1; j + 1 < T - 1; j += 2) {  // (+p, -p) rows: even part +- odd part
+    for (int j = pair0<M>(); j + 1 < T - 1; j += 2) {  // (+p, -p) rows: even part +- odd part
         const float e = dot_unit_first<T, SI, 0, 2>(tb.bt[j], in);
         const float s = os.s[j];
         const float o = dot_unit_first<T, SI, 1, 2>(tb.bt[j], in, s);
         if (s == 1.0f) {
             out[j * SO] = e + o;
-            out[(j + 1) * SO] = e - o;
+            out[(j + 1) * SO] = (pair_sign<M>() > 0.0f) ? e - o : o - e;
         } else {
             out[j * SO] = __builtin_fmaf(s, o, e);
-            out[(j + 1) * SO] = __builtin_fmaf(-s, o, e);
+            out[(j + 1) * SO] = (pair_sign<M>() > 0.0f) ? __builtin_fmaf(-s, o, e) : __builtin_fmaf(s, o, -e);
         }
     }
 }
@@ -207,20 +220,21 @@ template <int M, int SI, int SO>
 __device__ __forceinline__ void at_1d(const float *in, float *out) {
     constexpr Tables<M> tb{};
     constexpr int T = M + 2;
-    constexpr int NP = (T - 2) / 2;  // number of (+p, -p) pairs
+    constexpr int J0 = pair0<M>();
+    constexpr int NP = (T - 1 - J0) / 2;  // number of (+p, -p) pairs
     float s[NP], d[NP];
 #pragma unroll
     for (int q = 0; q < NP; ++q) {
-        s[q] = in[(1 + 2 * q) * SI] + in[(2 + 2 * q) * SI];
-        d[q] = in[(1 + 2 * q) * SI] - in[(2 + 2 * q) * SI];
+        s[q] = in[(J0 + 2 * q) * SI] + in[(J0 + 1 + 2 * q) * SI];
+        d[q] = in[(J0 + 2 * q) * SI] - in[(J0 + 1 + 2 * q) * SI];
     }
 #pragma unroll
     for (int i = 0; i < M; ++i) {
         float acc = 0.f;
         bool first = true;
-        mac(acc, first, tb.at[i][0], in[0]);
+        if constexpr (J0 == 1) mac(acc, first, tb.at[i][0], in[0]);
 #pragma unroll
-        for (int q = 0; q < NP; ++q) mac(acc, first, tb.at[i][1 + 2 * q], (i % 2 == 0) ? s[q] : d[q]);
+        for (int q = 0; q < NP; ++q) mac(acc, first, tb.at[i][J0 + 2 * q], (i % 2 == 0) ? s[q] : d[q]);
         mac(acc, first, tb.at[i][T - 1], in[(T - 1) * SI]);
         out[i * SO] = acc;
     }
@@ -254,6 +268,8 @@ __device__ __forceinline__ void input_tile_transform_emit(const float *d, Emit &
         for (int f4 = (i * T) / 4; f4 < ((i + 1) * T) / 4; ++f4)      // float4s completed by row i
             emit(f4, u[4 * f4], u[4 * f4 + 1], u[4 * f4 + 2], u[4 * f4 + 3]);
     }
+    // odd T: the last float4 holds the last frequency and three zeros
+    if constexpr ((T * T) % 4 == 1) emit((T * T) / 4, u[T * T - 1], 0.0f, 0.0f, 0.0f);
 }
 
 // Y = A^T Mm A for a T x T tile Mm (row-major); Y is M x M row-major.
@@ -276,23 +292,24 @@ template <int M, int SI, int SO, unsigned ROWS>
 __device__ __forceinline__ void at_1d_rows(const float *in, float *out) {
     constexpr Tables<M> tb{};
     constexpr int T = M + 2;
-    constexpr int NP = (T - 2) / 2;
+    constexpr int J0 = pair0<M>();
+    constexpr int NP = (T - 1 - J0) / 2;
     float s[NP], d[NP];
 #pragma unroll
     for (int q = 0; q < NP; ++q) {
-        if ((ROWS >> (1 + 2 * q)) & 1u) {
-            s[q] = in[(1 + 2 * q) * SI] + in[(2 + 2 * q) * SI];
-            d[q] = in[(1 + 2 * q) * SI] - in[(2 + 2 * q) * SI];
+        if ((ROWS >> (J0 + 2 * q)) & 1u) {
+            s[q] = in[(J0 + 2 * q) * SI] + in[(J0 + 1 + 2 * q) * SI];
+            d[q] = in[(J0 + 2 * q) * SI] - in[(J0 + 1 + 2 * q) * SI];
         }
     }
 #pragma unroll
     for (int i = 0; i < M; ++i) {
         float acc = 0.f;
         bool first = true;
-        if (ROWS & 1u) mac(acc, first, tb.at[i][0], in[0]);
+        if (J0 == 1 && (ROWS & 1u)) mac(acc, first, tb.at[i][0], in[0]);
 #pragma unroll
         for (int q = 0; q < NP; ++q)
-            if ((ROWS >> (1 + 2 * q)) & 1u) mac(acc, first, tb.at[i][1 + 2 * q], (i % 2 == 0) ? s[q] : d[q]);
+            if ((ROWS >> (J0 + 2 * q)) & 1u) mac(acc, first, tb.at[i][J0 + 2 * q], (i % 2 == 0) ? s[q] : d[q]);
         if ((ROWS >> (T - 1)) & 1u) mac(acc, first, tb.at[i][T - 1], in[(T - 1) * SI]);
         out[i * SO] = first ? 0.0f : acc;
     }
@@ -301,7 +318,7 @@ __device__ __forceinline__ void at_1d_rows(const float *in, float *out) {
 template <int M, unsigned ROWS>
 constexpr bool rows_pair_closed() {
     constexpr int T = M + 2;
-    for (int j = 1; j + 1 < T - 1; j += 2)
+    for (int j = pair0<M>(); j + 1 < T - 1; j += 2)
         if (((ROWS >> j) & 1u) != ((ROWS >> (j + 1)) & 1u)) return false;
     return true;
 }

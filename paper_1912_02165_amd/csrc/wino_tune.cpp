@@ -25,13 +25,13 @@ struct Choice {
 std::mutex g_mu;
 std::map<Key, Choice> g_table;
 
-constexpr unsigned kMBits = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M6;
+constexpr unsigned kMBits = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M5 | WINO_TUNE_M6;
 constexpr unsigned kAllBits = kMBits | WINO_TUNE_THREE_STAGE;
 
 bool mask_ok(unsigned c) { return (c & ~kAllBits) == 0 && (c & kMBits) != 0; }
 
 bool choice_ok(unsigned c, int m, int algo) {
-    if (m != 2 && m != 4 && m != 6) return false;
+    if (m != 2 && m != 4 && m != 5 && m != 6) return false;
     if (!(c & (1u << m))) return false;
     if (algo == WINO_ALGO_THREE_STAGE) return (c & WINO_TUNE_THREE_STAGE) != 0;
     return algo == WINO_ALGO_FUSED;
@@ -137,7 +137,7 @@ wino_plan *wino_conv_plan_tuned(int N, int C, int K, int H, int W, unsigned cand
     if (best.m == 0) {
         Buffers b;
         bool have_buffers = false;
-        for (int m : {2, 4, 6}) {
+        for (int m : {2, 4, 5, 6}) {
             if (!(candidates & (1u << m))) continue;
             for (int algo : {WINO_ALGO_FUSED, WINO_ALGO_THREE_STAGE}) {
                 if (algo == WINO_ALGO_THREE_STAGE && !(candidates & WINO_TUNE_THREE_STAGE)) continue;

@@ -47,8 +47,9 @@ SIGNATURES = {
     "wino_wisdom_size": (_i, []),
 }
 
-WINO_TUNE_M2, WINO_TUNE_M4, WINO_TUNE_M6, WINO_TUNE_THREE_STAGE = 1 << 2, 1 << 4, 1 << 6, 1 << 8
-WINO_TUNE_ALL_M = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M6
+WINO_TUNE_M2, WINO_TUNE_M4, WINO_TUNE_M5, WINO_TUNE_M6 = 1 << 2, 1 << 4, 1 << 5, 1 << 6
+WINO_TUNE_THREE_STAGE = 1 << 8
+WINO_TUNE_ALL_M = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M5 | WINO_TUNE_M6
 
 
 WINO_SCHED_AUTO, WINO_SCHED_SHARED, WINO_SCHED_PER_WAVE = 0, 1, 2

@@ -62,9 +62,15 @@ def test_bad_sizes(lib, args):
     assert "sizes must be >= 1" in msg
 
 
-@pytest.mark.parametrize("m", [0, 1, 3, 5, 7, 8])
+@pytest.mark.parametrize("m", [0, 1, 3, 7, 8])
 def test_bad_m(lib, m):
     assert "only F(2x2" in _plan_fails(lib, 1, 4, 4, 8, 8, m, wino.WINO_ALGO_FUSED, None)
+
+
+def test_f5_only_specialised(lib):
+    """F(5) is built for the warp-specialised fused kernel only."""
+    t = wino.WinoTuning(schedule=wino.WINO_SCHED_SHARED)
+    assert "not built" in _plan_fails(lib, 1, 4, 4, 8, 8, 5, wino.WINO_ALGO_FUSED, ctypes.byref(t))
 
 
 def test_too_large(lib):

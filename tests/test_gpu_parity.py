@@ -48,7 +48,7 @@ def rand(shape, seed):
 
 
 @pytest.mark.parametrize("algo", ALGOS)
-@pytest.mark.parametrize("m", (2, 4, 6))
+@pytest.mark.parametrize("m", (2, 4, 5, 6))
 @pytest.mark.parametrize("shape", SMALL, ids=lambda s: "x".join(map(str, s)))
 def test_small_shapes(algo, m, shape):
     N, C, K, H, W = shape
@@ -59,7 +59,7 @@ def test_small_shapes(algo, m, shape):
 
 
 @pytest.mark.parametrize("algo", ALGOS)
-@pytest.mark.parametrize("m", (2, 4))
+@pytest.mark.parametrize("m", (2, 4, 5))
 def test_layer1_full(algo, m):
     layer = workloads.LAYER_BY_ID[1]
     x, w = workloads.layer_inputs(layer)
@@ -97,7 +97,7 @@ def test_full_layers_sampled(algo, pair):
     print(f"rel_l2={rel:.3e} max={mx:.3e} over {len(planes)} planes")
 
 
-@pytest.mark.parametrize("m", (2, 4, 6))
+@pytest.mark.parametrize("m", (2, 4, 5, 6))
 def test_three_stage_intermediates(m):
     """Each unfused stage against the fp64 CPU Winograd's matching intermediate."""
     from oracle import winograd
@@ -116,9 +116,13 @@ def test_three_stage_intermediates(m):
     U_ref = winograd.input_transform(x, m)               # (T2, C, ntiles)
     M_ref = winograd.frequency_gemm(U_ref, Wt_ref)       # (T2, K, ntiles)
     ntiles = U_ref.shape[2]
-    # undo the operand order: [kb][cs][f/4][lane][f%4], lane = (c%4)*16 + k%16
-    Kb, Cs = wt.shape[:2]
-    flat = wt.reshape(Kb, Cs, T2 // 4, 64, 4)
+    # undo the operand order: [kb][cs][f/4][lane][f%4], lane = (c%4)*16 + k%16; the
+    # frequency dim is padded to whole float4s (F(5): 49 -> 52) with zeros
+    Kb, Cs, T2P = wt.shape[:3]
+    assert T2P == (T2 + 3) // 4 * 4
+    flat = wt.reshape(Kb, Cs, T2P // 4, 64, 4)
+    for f in range(T2, T2P):
+        assert not flat[:, :, f // 4, :, f % 4].any()
     wt_fck = np.empty((T2, Cs * 4, Kb * 16), np.float32)
     for f in range(T2):
         blk = flat[:, :, f // 4, :, f % 4].reshape(Kb, Cs, 4, 16)   # kb, cs, c%4, k%16
@@ -135,7 +139,7 @@ def test_three_stage_intermediates(m):
     assert_close(y.cpu().numpy(), direct_conv(x, w), m, "three-stage end to end")
 
 
-@pytest.mark.parametrize("m", (2, 4, 6))
+@pytest.mark.parametrize("m", (2, 4, 5, 6))
 def test_plan_reused_across_calls(m):
     """One plan, several calls: split items' arrival counters are back at zero after
     every call, so each call is correct and bitwise equal to the first."""
@@ -236,7 +240,7 @@ def test_bad_pointers_rejected():
         hip.hipFree(ptr)
 
 
-@pytest.mark.parametrize("m", (2, 4, 6))
+@pytest.mark.parametrize("m", (2, 4, 5, 6))
 def test_unaligned_input_pointer(m):
     """x starting 4 bytes past an aligned address takes the per-element load path."""
     N, C, K, H, W = 2, 9, 20, 16, 24
