@@ -168,26 +168,35 @@ __device__ __forceinline__ float dot_unit_first(const float (&c)[T], const float
     return acc;
 }
 
-// Per row j of B^T: the magnitude shared by all nonzero odd-column entries, or 1
-// if they differ.  The odd part of a (+p, -p) row pair can then be summed with
-// +-1 coefficients and the magnitude applied once per output.
+// Per row j of B^T and parity (0: even columns, 1: odd columns): a scale by which
+// that half of the row is divided so that its sum starts with a coefficient of
+// +-1 (no separate multiply), or 1 if the half already has one or is empty.  Only
+// powers of two are used, so scaling is exact in fp32.
 template <int M>
-struct OddScale {
-    float s[M + 2];
-    constexpr OddScale() : s{} {
+struct HalfScale {
+    float s[M + 2][2];
+    static constexpr bool pow2(float c) {
+        if (c <= 0.0f) return false;
+        while (c < 1.0f) c *= 2.0f;
+        while (c > 1.0f) c *= 0.5f;
+        return c == 1.0f;
+    }
+    constexpr HalfScale() : s{} {
         constexpr int T = M + 2;
         Tables<M> tb{};
-        for (int j = 0; j < T; ++j) {
-            float m = 0.0f;
-            bool same = true;
-            for (int a = 1; a < T; a += 2) {
-                const float c = tb.bt[j][a] < 0.0f ? -tb.bt[j][a] : tb.bt[j][a];
-                if (c == 0.0f) continue;
-                if (m == 0.0f) m = c;
-                else if (m != c) same = false;
+        for (int j = 0; j < T; ++j)
+            for (int par = 0; par < 2; ++par) {
+                bool unit = false, any = false;
+                float pick = 1.0f;
+                for (int a = par; a < T; a += 2) {
+                    const float c = tb.bt[j][a] < 0.0f ? -tb.bt[j][a] : tb.bt[j][a];
+                    if (c == 0.0f) continue;
+                    any = true;
+                    if (c == 1.0f) unit = true;
+                    else if (pick == 1.0f && pow2(c)) pick = c;
+                }
+                s[j][par] = (!any || unit) ? 1.0f : pick;
             }
-            s[j] = (same && m != 0.0f) ? m : 1.0f;
-        }
     }
 };
 
@@ -195,22 +204,31 @@ struct OddScale {
 template <int M, int SI, int SO>
 __device__ __forceinline__ void bt_1d(const float *in, float *out) {
     constexpr Tables<M> tb{};
-    constexpr OddScale<M> os{};
+    constexpr HalfScale<M> hs{};
     constexpr int T = M + 2;
+    constexpr bool neg = pair_sign<M>() < 0.0f;
     // p = 0 (even T) and the point at infinity: plain rows
     if constexpr (pair0<M>() == 1) out[0] = dot_unit_first<T, SI, 0, 1>(tb.bt[0], in);
     out[(T - 1) * SO] = dot_unit_first<T, SI, 0, 1>(tb.bt[T - 1], in);
 #pragma unroll
-    for (int j = pair0<M>(); j + 1 < T - 1; j += 2) {  // (+p, -p) rows: even part +- odd part
-        const float e = dot_unit_first<T, SI, 0, 2>(tb.bt[j], in);
-        const float s = os.s[j];
-        const float o = dot_unit_first<T, SI, 1, 2>(tb.bt[j], in, s);
-        if (s == 1.0f) {
-            out[j * SO] = e + o;
-            out[(j + 1) * SO] = (pair_sign<M>() > 0.0f) ? e - o : o - e;
+    for (int j = pair0<M>(); j + 1 < T - 1; j += 2) {
+        // (+p, -p) rows: row j = E + O, row j+1 = +-(E - O) with E, O the sums over
+        // its even and odd columns, E = se * e and O = so * o
+        const float se = hs.s[j][0], so = hs.s[j][1];
+        const float e0 = dot_unit_first<T, SI, 0, 2>(tb.bt[j], in, se);
+        const float o0 = dot_unit_first<T, SI, 1, 2>(tb.bt[j], in, so);
+        // both halves scaled: apply the even scale by itself (one multiply)
+        const float e = (se != 1.0f && so != 1.0f) ? se * e0 : e0;
+        const float es = (se != 1.0f && so != 1.0f) ? 1.0f : se;
+        if (es == 1.0f && so == 1.0f) {
+            out[j * SO] = e + o0;
+            out[(j + 1) * SO] = neg ? o0 - e : e - o0;
+        } else if (es == 1.0f) {
+            out[j * SO] = __builtin_fmaf(so, o0, e);
+            out[(j + 1) * SO] = neg ? __builtin_fmaf(so, o0, -e) : __builtin_fmaf(-so, o0, e);
         } else {
-            out[j * SO] = __builtin_fmaf(s, o, e);
-            out[(j + 1) * SO] = (pair_sign<M>() > 0.0f) ? __builtin_fmaf(-s, o, e) : __builtin_fmaf(s, o, -e);
+            out[j * SO] = __builtin_fmaf(es, e, o0);
+            out[(j + 1) * SO] = neg ? __builtin_fmaf(-es, e, o0) : __builtin_fmaf(es, e, -o0);
         }
     }
 }
