@@ -17,7 +17,9 @@ the host cores.
 --all adds a per-(layer, m, algorithm) table (stderr, and --out): back-to-back step
 time, the median of single calls warm and cold (a 512 MB scratch write before each
 cold call evicts L2 and the Infinity Cache), and the transform-domain kernel time;
-plus, per layer, the m and algorithm a tuned plan picks (algo "tuned").
+plus, per layer, the m and algorithm a tuned plan picks (algo "tuned"), and on
+layers with C >= 128 the fused kernel with every work item split into 2 and 4
+channel pieces (algo "fused_csplitP").
 """
 
 import argparse
@@ -87,7 +89,7 @@ def rep_times(p, x, w, y, steps, stream, scratch=None):
     return sorted(times)[len(times) // 2]
 
 
-def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False):
+def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False, tuning=None):
     """Time `steps` steps; returns dict with ms_per_step and the transform-domain
     kernel's average duration (ms) measured between events on the same stream.
     per_call: also the median time of single calls, warm and cold (after a 512 MB
@@ -97,7 +99,7 @@ def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False):
     N, C, K, H, W = layer.N, layer.C, layer.K, layer.H, layer.W
     y = torch.empty((N, K, H, W), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
-    with wc.Plan(N, C, K, H, W, m, algo) as p:
+    with wc.Plan(N, C, K, H, W, m, algo, tuning) as p:
         for _ in range(warmup):
             p.run(x, w, y)
         torch.cuda.synchronize()
@@ -225,8 +227,15 @@ def main():
                                    wc.WINO_TUNE_ALL_M | wc.WINO_TUNE_THREE_STAGE)
                 cases.append((tp.m, tp.algo, "tuned"))
                 tp.close()
+            if lay.C >= 128:
+                # every work item split into channel pieces (partial outputs added)
+                cases += [(mm, "fused", "fused_csplit%d" % P) for P in (2, 4)]
             for m_c, algo, label in cases:
-                r = time_pair(lay, m_c, algo, args.steps, args.warmup, xa, wa, per_call=True)
+                tuning = None
+                if label.startswith("fused_csplit"):
+                    tuning = {"channel_splits": int(label[len("fused_csplit"):])}
+                r = time_pair(lay, m_c, algo, args.steps, args.warmup, xa, wa, per_call=True,
+                              tuning=tuning)
                 row = {"workload": lay.tag(m_c), "algo": label, "ms_per_step": r["ms_per_step"],
                        "eff_tflops": r["direct_flops"] / (r["ms_per_step"] * 1e-3) / 1e12,
                        "warm_call_ms_median": r["warm_call_ms_median"],

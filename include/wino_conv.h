@@ -85,12 +85,28 @@ enum {
  *   k_blocks_per_wave: per-wave schedule: output channels per wave, in blocks of 16.
  *   waves_per_group:   per-wave schedule: waves (16 tiles each) per workgroup, 1..4.
  *   tile_blocks:       shared schedule: tiles per workgroup in blocks of 16 (1, or 2
- *                      for m <= 4). */
+ *                      for m <= 4).
+ *   channel_splits:    specialised schedule (fused algorithm only): compute the
+ *                      layer as P convolutions over disjoint, consecutive subsets
+ *                      of the input channels and add their outputs (Sec. 7 on
+ *                      splitting channels; the output transform is linear, so each
+ *                      subset's products are inverse-transformed on their own).
+ *                      Every work item (16 tiles x 64 output channels; 32 tiles
+ *                      for m = 2, 32 channels for m >= 5) is cut into pieces of L = ceil(S / channel_splits)
+ *                      channel stages, S = ceil(C / 16) (ceil(C / 8) for m = 2),
+ *                      so P = ceil(S / L) pieces, at most S.  The pieces' outputs
+ *                      go to a plan-owned buffer of P partial tiles per item and
+ *                      are added in channel order by the piece that finishes last
+ *                      (results do not depend on the order pieces run in, but
+ *                      differ from the unsplit sum by rounding).  0 or 1: no
+ *                      split; at most WINO_MAX_CHANNEL_SPLITS. */
+#define WINO_MAX_CHANNEL_SPLITS 64
 typedef struct {
     int schedule;
     int k_blocks_per_wave;
     int waves_per_group;
     int tile_blocks;
+    int channel_splits;
 } wino_tuning;
 
 /* Create a plan for an F(m x m, 3 x 3) convolution of an N x C x H x W input

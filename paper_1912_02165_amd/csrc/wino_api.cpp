@@ -212,7 +212,7 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
     FusedCfg cfg = wino::fused_cfg_default(g);
     if (t) {
         if (t->schedule < 0 || t->k_blocks_per_wave < 0 || t->waves_per_group < 0 ||
-            t->tile_blocks < 0) {
+            t->tile_blocks < 0 || t->channel_splits < 0) {
             set_err("tuning fields must be >= 0");
             return nullptr;
         }
@@ -220,6 +220,18 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         if (t->k_blocks_per_wave) cfg.nkb = t->k_blocks_per_wave;
         if (t->waves_per_group) cfg.waves = t->waves_per_group;
         if (t->tile_blocks) cfg.tb = t->tile_blocks;
+        if (t->channel_splits > 1) {
+            if (algo != WINO_ALGO_FUSED || cfg.schedule != wino::kSchedSpecialised) {
+                set_err("channel_splits=%d needs the fused algorithm with the specialised schedule",
+                        t->channel_splits);
+                return nullptr;
+            }
+            if (t->channel_splits > WINO_MAX_CHANNEL_SPLITS) {
+                set_err("channel_splits=%d exceeds %d", t->channel_splits, WINO_MAX_CHANNEL_SPLITS);
+                return nullptr;
+            }
+            cfg.csplit = t->channel_splits;
+        }
     }
     if (algo == WINO_ALGO_FUSED && !wino::fused_cfg_supported(m, cfg)) {
         set_err("fused schedule %d (k_blocks_per_wave=%d waves_per_group=%d tile_blocks=%d) "
@@ -300,9 +312,9 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
     if (log_enabled())
         fprintf(stderr,
                 "[wino] plan N=%d C=%d K=%d H=%d W=%d m=%d algo=%s tiles=%d schedule=%d tb=%d "
-                "nkb=%d waves=%d workspace=%zu B\n",
+                "nkb=%d waves=%d channel_splits=%d workspace=%zu B\n",
                 N, C, K, H, W, m, algo == WINO_ALGO_FUSED ? "fused" : "three_stage", g.ntiles,
-                cfg.schedule, cfg.tb, cfg.nkb, cfg.waves, total_bytes);
+                cfg.schedule, cfg.tb, cfg.nkb, cfg.waves, cfg.csplit, total_bytes);
     return p;
 oom:
     (void)hipGetLastError();

@@ -28,18 +28,20 @@ struct FusedCfg {
     int nkb;       // per-wave: 16-channel output blocks per wave
     int waves;     // per-wave: waves per workgroup (each owns 16 tiles)
     int num_cus;   // compute units of the device (persistent grid size)
+    int csplit;    // specialised: channel pieces per work item (0 or 1: whole items)
 };
 
-// Split plan of the warp-specialised fused kernel: the last round of items is
-// divided stage-wise among all workgroups; each split item's partial outputs
-// go to a plan-owned buffer and are added by the contributor that finishes last.
+// Split plan of the warp-specialised fused kernel: the last round of items (or,
+// with channel splitting, every item) is divided stage-wise among workgroups;
+// each split item's partial outputs go to a plan-owned buffer and are added by
+// the contributor that finishes last.
 struct SplitInfo {
     int grid;              // workgroups launched
     int n_items, n_kgroups, stages;
     int nfull;             // full rounds of whole items (n_items / grid)
     int tail_first, n_tail;  // items [0, tail_first) are whole, the n_tail after are split
-    unsigned tail_units;   // n_tail * stages
-    unsigned piece;        // stages per piece of a split item
+    int n_units;           // n_tail * maxc pieces
+    int piece;             // stages per piece of a split item (the last piece may be shorter)
     int maxc;              // contributors (pieces) per split item
     int part_floats;       // floats of one contributor's partial output
 };

@@ -837,12 +837,15 @@ __device__ __forceinline__ ItemRange item_range(int n_items) {
 // Work of one persistent workgroup of the warp-specialised kernel, as one
 // sequence of (item, channel stage) pairs shared by its producers and consumers:
 // first its whole items (taken as by item_range from the first n_whole items),
-// then at most one piece of a split item: each remaining item is cut into P
-// pieces of equal stage ranges ("split units" [b*L, (b+1)*L) of the remaining
-// items' stages for workgroup b, L = stages / P), which spreads a last round that
-// would otherwise leave compute units idle.  A workgroup's sequence falls into
-// segments, one per item it works on; a piece of a split item yields a partial
-// output, and the partial outputs of an item are added by whichever of its P
+// then its pieces of split items.  Each split item is cut into P pieces of L
+// consecutive channel stages (the last one shorter when L does not divide the
+// stages); the pieces ("split units", unit u is piece u % P of split item u / P)
+// are distributed as by item_range.  Splitting only the items of a last, partly
+// filled round spreads that round over compute units that would otherwise idle;
+// splitting every item computes the layer as P convolutions over subsets of the
+// input channels whose outputs are added (Sec. 7).  A workgroup's sequence falls
+// into segments, one per whole item or piece; a piece yields a partial output,
+// and the partial outputs of an item are added by whichever of its P
 // contributors finishes last.
 // Item numbering of the warp-specialised kernel: with KM false the output-channel
 // group varies fastest (items = tile groups x groups, the groups of one tile group
@@ -857,20 +860,21 @@ __device__ __forceinline__ int item_kgroup(int it, int n_inner) { return KM ? it
 struct WsSplit {
     int n_whole;          // items distributed whole (item_range over the first n_whole)
     int tail_first;       // first split item
-    unsigned tail_units;  // split items x stages per item
-    unsigned piece;       // stages per piece of a split item (L)
+    int n_units;          // split items x P
+    int P;                // pieces per split item (contributors)
+    int piece;            // stages per piece (L)
     float *part;          // partial outputs, [split item][contributor][part_floats]
     unsigned *cnt;        // contributors arrived, per split item (zero between calls)
-    int maxc;             // contributor slots per split item
     int part_floats;      // floats of one partial output
 };
 
 struct WsSeq {
-    int first, stride, nfull;  // whole items first + i * stride, i < nfull
-    int S;                     // stages per item
+    int first, stride, nfull;     // whole items first + i * stride, i < nfull
+    int pfirst, pstride, npiece;  // split units pfirst + i * pstride, i < npiece
+    int S;                        // stages per item
     int n_items;
-    int titem, tsb, tse;       // the piece of a split item, stages [tsb, tse) (none if equal)
-    int nseg;                  // segments: nfull whole items, then the piece
+    int tail_first, P, L;         // as in WsSplit
+    int nseg;                     // segments: nfull whole items, then npiece pieces
 
     __device__ __forceinline__ void init(const WsSplit &sp, int n_items_, int stages, bool split) {
         S = stages;
@@ -879,19 +883,30 @@ struct WsSeq {
         first = ir.first;
         stride = ir.stride;
         nfull = ir.count;
-        // workgroup b's piece is split units [b*L, b*L + L): pieces never straddle items
-        const unsigned long long a = (unsigned long long)blockIdx.x * sp.piece;
-        titem = n_items;
-        tsb = tse = 0;
-        if (split && a < sp.tail_units) {
-            const unsigned t = (unsigned)a / (unsigned)S;
-            titem = sp.tail_first + (int)t;
-            tsb = (int)((unsigned)a - t * (unsigned)S);
-            tse = tsb + (int)sp.piece;
+        pfirst = 0;
+        pstride = 1;
+        npiece = 0;
+        tail_first = sp.tail_first;
+        P = sp.P > 0 ? sp.P : 1;
+        L = sp.piece > 0 ? sp.piece : stages;
+        if (split) {
+            const ItemRange pr = item_range(sp.n_units);
+            pfirst = pr.first;
+            pstride = pr.stride;
+            npiece = pr.count;
         }
-        nseg = nfull + (tse > tsb ? 1 : 0);
+        nseg = nfull + npiece;
     }
-    __device__ __forceinline__ int length() const { return nfull * S + (tse - tsb); }
+    __device__ __forceinline__ int length() const {
+        // stages of the pieces: L each, except those that are the last of their item
+        int n = nfull * S;
+        for (int i = 0; i < npiece; ++i) {
+            int item, sb, se;
+            segment(nfull + i, item, sb, se);
+            n += se - sb;
+        }
+        return n;
+    }
     __device__ __forceinline__ int segments() const { return nseg; }
     // segment k: item and its stages [sb, se); k past the end repeats the last one
     __device__ __forceinline__ void segment(int k, int &item, int &sb, int &se) const {
@@ -901,9 +916,11 @@ struct WsSeq {
             sb = 0;
             se = S;
         } else {
-            item = titem;
-            sb = tsb;
-            se = tse;
+            const int u = pfirst + (k - nfull) * pstride;
+            const int t = u / P;
+            item = tail_first + t;
+            sb = (u - t * P) * L;
+            se = sb + L < S ? sb + L : S;
         }
     }
     // A walker over the sequence, one stage at a time.
@@ -1167,11 +1184,10 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
         const float *pbase = sp.part;
         int32x4 mine{};
         if (partial) {
-            // the item's pieces belong to workgroups b0 .. b0 + P - 1, in stage order
-            const int b0 = (int)(t_split * (unsigned)sq.S / sp.piece);
-            ncontrib = sp.maxc;
-            pbase = sp.part + (long long)t_split * sp.maxc * sp.part_floats;
-            mine = make_rsrc_uniform(pbase + (long long)((int)blockIdx.x - b0) * sp.part_floats,
+            // contributor index: the piece's position in stage order
+            ncontrib = sq.P;
+            pbase = sp.part + (long long)t_split * sq.P * sp.part_floats;
+            mine = make_rsrc_uniform(pbase + (long long)(sb / sq.L) * sp.part_floats,
                                      (unsigned)sp.part_floats * 4u);
         }
         out_tiles([&](int t, int v, int k_out, const TileIdx &ti, const float *yy) {
@@ -1719,6 +1735,7 @@ FusedCfg fused_cfg_default(const Geometry &g) {
     c.num_cus = 256;  // replaced by the device's count at plan time
     c.tb = (g.m == 2) ? 2 : 1;
     c.waves = 4;
+    c.csplit = 0;
     switch (g.m) {
         case 2: c.nkb = g.Kb >= 4 ? 4 : (g.Kb >= 2 ? 2 : 1); break;
         case 4: c.nkb = g.Kb >= 2 ? 2 : 1; break;
@@ -1729,8 +1746,10 @@ FusedCfg fused_cfg_default(const Geometry &g) {
 
 // Split plan of the warp-specialised kernel (see WsSeq): grid size, whole items
 // per workgroup, the split items and the partial-output buffer they need.
+// csplit > 1 splits every item into that many channel pieces (at most one per
+// stage); otherwise only a last, partly filled round may be split.
 template <int M, int TB, int FS>
-static SplitInfo ws_split_info(const Geometry &g, int num_cus) {
+static SplitInfo ws_split_info(const Geometry &g, int num_cus, int csplit) {
     constexpr int R = 16 * TB, CC = 256 / R, KBW = 4 / FS;
     SplitInfo si{};
     const int n_tgroups = (g.ntiles + R - 1) / R;
@@ -1743,9 +1762,24 @@ static SplitInfo ws_split_info(const Geometry &g, int num_cus) {
     si.part_floats = KBW * TB * 4 * ((M * M + 3) / 4 * 4) * 64;  // output tiles padded to float4s
     si.tail_first = si.n_items;  // every item whole unless split below
     si.n_tail = 0;
-    si.tail_units = 0;
-    si.piece = (unsigned)si.stages;
+    si.n_units = 0;
+    si.piece = si.stages;
     si.maxc = 0;
+    if (csplit > 1 && si.stages > 1) {
+        // every item in P pieces of L stages: L = ceil(stages / csplit), P =
+        // ceil(stages / L) (P < csplit when csplit does not divide the stages)
+        const int want = csplit < si.stages ? csplit : si.stages;
+        const int L = (si.stages + want - 1) / want;
+        const int P = (si.stages + L - 1) / L;
+        si.nfull = 0;
+        si.tail_first = 0;
+        si.n_tail = si.n_items;
+        si.piece = L;
+        si.maxc = P;
+        si.n_units = si.n_items * P;
+        si.grid = si.n_units < cus ? si.n_units : cus;
+        return si;
+    }
     // Split the items of a last, partly filled round into P pieces (P <= 4,
     // dividing the stages) when at least half of the compute units would idle in
     // it otherwise.  A piece costs its workgroup a partial-output epilogue
@@ -1760,8 +1794,8 @@ static SplitInfo ws_split_info(const Geometry &g, int num_cus) {
     if (P < 2) return si;
     si.tail_first = si.nfull * cus;
     si.n_tail = tail;
-    si.piece = (unsigned)(si.stages / P);
-    si.tail_units = (unsigned)tail * (unsigned)si.stages;
+    si.piece = si.stages / P;
+    si.n_units = tail * P;
     si.maxc = P;
     si.grid = si.nfull > 0 ? cus : tail * P;
     return si;
@@ -1770,25 +1804,25 @@ static SplitInfo ws_split_info(const Geometry &g, int num_cus) {
 SplitInfo fused_split_info(const Geometry &g, const FusedCfg &cfg) {
     if (cfg.schedule != kSchedSpecialised) return SplitInfo{};
     switch (g.m) {
-        case 2: return ws_split_info<2, 2, 1>(g, cfg.num_cus);
-        case 4: return ws_split_info<4, 1, 1>(g, cfg.num_cus);
-        case 5: return ws_split_info<5, 1, 2>(g, cfg.num_cus);
-        default: return ws_split_info<6, 1, 2>(g, cfg.num_cus);
+        case 2: return ws_split_info<2, 2, 1>(g, cfg.num_cus, cfg.csplit);
+        case 4: return ws_split_info<4, 1, 1>(g, cfg.num_cus, cfg.csplit);
+        case 5: return ws_split_info<5, 1, 2>(g, cfg.num_cus, cfg.csplit);
+        default: return ws_split_info<6, 1, 2>(g, cfg.num_cus, cfg.csplit);
     }
 }
 
 template <int M, int TB, int FS>
 static void launch_ws_t(const Geometry &g, const float *x, const float *wt, float *y, bool vec,
-                        int num_cus, const SplitBuffers &sb, hipStream_t s) {
-    const SplitInfo si = ws_split_info<M, TB, FS>(g, num_cus);
+                        int num_cus, int csplit, const SplitBuffers &sb, hipStream_t s) {
+    const SplitInfo si = ws_split_info<M, TB, FS>(g, num_cus, csplit);
     WsSplit sp;
     sp.n_whole = si.tail_first;
     sp.tail_first = si.tail_first;
-    sp.tail_units = si.tail_units;
+    sp.n_units = si.n_units;
+    sp.P = si.maxc;
     sp.piece = si.piece;
     sp.part = sb.part;
     sp.cnt = sb.cnt;
-    sp.maxc = si.maxc;
     sp.part_floats = si.part_floats;
     dim3 block(512), grid((unsigned)si.grid);
     // row-vector input loads need every row start aligned to the vector width
@@ -1868,10 +1902,10 @@ hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, 
     }
     if (cfg.schedule == kSchedSpecialised) {
         switch (g.m) {
-            case 2: launch_ws_t<2, 2, 1>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
-            case 4: launch_ws_t<4, 1, 1>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
-            case 5: launch_ws_t<5, 1, 2>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
-            default: launch_ws_t<6, 1, 2>(g, x, wt, y, vec, cfg.num_cus, sb, s); break;
+            case 2: launch_ws_t<2, 2, 1>(g, x, wt, y, vec, cfg.num_cus, cfg.csplit, sb, s); break;
+            case 4: launch_ws_t<4, 1, 1>(g, x, wt, y, vec, cfg.num_cus, cfg.csplit, sb, s); break;
+            case 5: launch_ws_t<5, 1, 2>(g, x, wt, y, vec, cfg.num_cus, cfg.csplit, sb, s); break;
+            default: launch_ws_t<6, 1, 2>(g, x, wt, y, vec, cfg.num_cus, cfg.csplit, sb, s); break;
         }
         return hipGetLastError();
     }

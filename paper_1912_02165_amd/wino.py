@@ -54,11 +54,13 @@ WINO_TUNE_ALL_M = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M5 | WINO_TUNE_M6
 
 WINO_SCHED_AUTO, WINO_SCHED_SHARED, WINO_SCHED_PER_WAVE = 0, 1, 2
 WINO_SCHED_SPECIALISED, WINO_SCHED_PERSISTENT = 3, 4
+WINO_MAX_CHANNEL_SPLITS = 64
 
 
 class WinoTuning(ctypes.Structure):
     _fields_ = [("schedule", ctypes.c_int), ("k_blocks_per_wave", ctypes.c_int),
-                ("waves_per_group", ctypes.c_int), ("tile_blocks", ctypes.c_int)]
+                ("waves_per_group", ctypes.c_int), ("tile_blocks", ctypes.c_int),
+                ("channel_splits", ctypes.c_int)]
 
 
 class WinoError(RuntimeError):

@@ -92,6 +92,30 @@ def test_bad_tuning(lib):
     assert ">= 0" in _plan_fails(lib, 1, 4, 4, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
 
 
+def test_tuning_struct_matches_header():
+    """The binding's wino_tuning has the header's fields, in order."""
+    with open(os.path.join(ROOT, "include", "wino_conv.h")) as f:
+        hdr = f.read()
+    body = re.search(r"typedef struct \{([^}]*)\} wino_tuning;", hdr).group(1)
+    fields = re.findall(r"int (\w+);", body)
+    assert fields == [f for f, _ in wino.WinoTuning._fields_]
+    limit = int(re.search(r"#define WINO_MAX_CHANNEL_SPLITS (\d+)", hdr).group(1))
+    assert limit == wino.WINO_MAX_CHANNEL_SPLITS
+
+
+def test_bad_channel_splits(lib):
+    """Channel splitting is checked before any device work: a negative count, a
+    count above the limit, another schedule or the three-stage algorithm."""
+    t = wino.WinoTuning(channel_splits=-2)
+    assert ">= 0" in _plan_fails(lib, 1, 64, 16, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+    t = wino.WinoTuning(channel_splits=wino.WINO_MAX_CHANNEL_SPLITS + 1)
+    assert "exceeds" in _plan_fails(lib, 1, 64, 16, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+    t = wino.WinoTuning(schedule=wino.WINO_SCHED_SHARED, channel_splits=2)
+    assert "specialised" in _plan_fails(lib, 1, 64, 16, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+    t = wino.WinoTuning(channel_splits=2)
+    assert "specialised" in _plan_fails(lib, 1, 64, 16, 8, 8, 4, wino.WINO_ALGO_THREE_STAGE, ctypes.byref(t))
+
+
 def test_forced_allocation_failure(lib, monkeypatch):
     monkeypatch.setenv("WINO_TEST_FAIL_ALLOC", "1")
     msg = _plan_fails(lib, 1, 4, 4, 8, 8, 4, wino.WINO_ALGO_THREE_STAGE, None)

@@ -214,6 +214,62 @@ def test_tuning_overrides_agree():
             assert_close(y.cpu().numpy(), ref, m, f"shared F({m}) tile_blocks={tb}")
 
 
+CSPLIT_SHAPES = [(1, 1, 1, 1, 1), (3, 8, 20, 17, 23), (2, 37, 45, 29, 35), (1, 64, 64, 20, 20),
+                 (1, 130, 18, 9, 10), (1, 32, 128, 8, 8)]
+
+
+@pytest.mark.parametrize("csplit", (2, 3, 64))
+@pytest.mark.parametrize("m", (2, 4, 5, 6))
+@pytest.mark.parametrize("shape", CSPLIT_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_channel_split_small(shape, m, csplit):
+    """Every work item cut into channel pieces whose partial outputs are added:
+    one-stage layers (nothing to split), ragged channel tails, more pieces asked
+    for than there are stages."""
+    N, C, K, H, W = shape
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=sum(shape) + 7 * m + csplit)
+    print(f"\n[gpu] channel split {csplit} m={m} shape={shape}", flush=True)
+    y = run_gpu(x, w, m, "fused", {"channel_splits": csplit}).cpu().numpy()
+    assert_close(y, direct_conv(x, w), m, f"F({m}) {shape} channel_splits={csplit}")
+
+
+CSPLIT_FULL = [(5, 6, 2), (5, 6, 4), (5, 4, 3), (4, 4, 2)]
+
+
+@pytest.mark.parametrize("case", CSPLIT_FULL, ids=lambda c: f"layer{c[0]}-F{c[1]}-split{c[2]}")
+def test_channel_split_full_layers_sampled(case):
+    lid, m, csplit = case
+    layer = workloads.LAYER_BY_ID[lid]
+    x, w = workloads.layer_inputs(layer)
+    print(f"\n[gpu] {layer.tag(m)} channel split {csplit} full size", flush=True)
+    y = run_gpu(x, w, m, "fused", {"channel_splits": csplit})
+    assert bool(torch.isfinite(y).all()), "non-finite output"
+    planes = sample_planes(layer.N, layer.K, seed=layer.id * 10 + m + 100 * csplit)
+    n_idx = torch.tensor([p[0] for p in planes], device="cuda")
+    k_idx = torch.tensor([p[1] for p in planes], device="cuda")
+    got = y[n_idx, k_idx].cpu().numpy()
+    ref = direct_conv_planes(x, w, planes)
+    rel, mx = assert_close(got, ref, m, f"{layer.tag(m)} channel_splits={csplit} planes {planes}")
+    print(f"rel_l2={rel:.3e} max={mx:.3e} over {len(planes)} planes")
+
+
+def test_channel_split_reproducible():
+    """Partial outputs are added in channel order whatever order the pieces
+    finish in, and the arrival counters are left at zero: repeated calls on one
+    plan give identical bits."""
+    N, C, K, H, W = 2, 96, 80, 18, 22
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=9)
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    ys = []
+    with wc.Plan(N, C, K, H, W, 4, "fused", {"channel_splits": 3}) as p:
+        for _ in range(3):
+            y = torch.full((N, K, H, W), float("nan"), device="cuda")
+            p.run(xd, wd, y)
+            ys.append(y)
+        torch.cuda.synchronize()
+    assert torch.equal(ys[0], ys[1]) and torch.equal(ys[0], ys[2])
+    assert_close(ys[0].cpu().numpy(), direct_conv(x, w), 4, "channel_splits=3 repeated")
+
+
 def test_bad_pointers_rejected():
     N, C, K, H, W = 1, 4, 4, 8, 8
     xd = torch.zeros((N, C, H, W), device="cuda")
