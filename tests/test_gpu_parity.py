@@ -77,7 +77,9 @@ def sample_planes(N, K, seed, count=8):
     return sorted(planes)
 
 
-FULL_PAIRS = [(l, m) for (l, m) in workloads.PAIRS if l.id != 1]
+# the configured pairs, plus the 14x14 C=K=512 layer at F(4) (the tile size a
+# tuned plan picks there; 4.5 rounds of work items, the last split into pieces)
+FULL_PAIRS = [(l, m) for (l, m) in workloads.PAIRS if l.id != 1] + [(workloads.LAYER_BY_ID[5], 4)]
 
 
 @pytest.mark.parametrize("algo", ALGOS)
