@@ -19,7 +19,9 @@ time, the median of single calls warm and cold (a 512 MB scratch write before ea
 cold call evicts L2 and the Infinity Cache), and the transform-domain kernel time;
 plus, per layer, the m and algorithm a tuned plan picks (algo "tuned"), and on
 layers with C >= 128 the fused kernel with every work item split into 2 and 4
-channel pieces (algo "fused_csplitP").
+channel pieces (algo "fused_csplitP"); and per layer the FFT-tile algorithm
+(algo "fft", 16 x 16 tiles; its "transform-domain" rate counts the real flops
+of its complex products).
 """
 
 import argparse
@@ -216,6 +218,7 @@ def main():
         import paper_1912_02165_amd as wc
         rows = []
         tuned_done = set()
+        fft_done = set()
         for lay, mm in workloads.PAIRS:
             xn, wn = workloads.layer_inputs(lay)
             xa, wa = torch.from_numpy(xn).cuda(), torch.from_numpy(wn).cuda()
@@ -230,13 +233,18 @@ def main():
             if lay.C >= 128:
                 # every work item split into channel pieces (partial outputs added)
                 cases += [(mm, "fused", "fused_csplit%d" % P) for P in (2, 4)]
+            if lay.id not in fft_done:
+                # the FFT-tile algorithm (16 x 16 tiles, m = 14), once per layer
+                fft_done.add(lay.id)
+                cases.append((14, "fft", "fft"))
             for m_c, algo, label in cases:
                 tuning = None
                 if label.startswith("fused_csplit"):
                     tuning = {"channel_splits": int(label[len("fused_csplit"):])}
                 r = time_pair(lay, m_c, algo, args.steps, args.warmup, xa, wa, per_call=True,
                               tuning=tuning)
-                row = {"workload": lay.tag(m_c), "algo": label, "ms_per_step": r["ms_per_step"],
+                wl = lay.name + "/FFT(16x16 tiles)" if algo == "fft" else lay.tag(m_c)
+                row = {"workload": wl, "algo": label, "ms_per_step": r["ms_per_step"],
                        "eff_tflops": r["direct_flops"] / (r["ms_per_step"] * 1e-3) / 1e12,
                        "warm_call_ms_median": r["warm_call_ms_median"],
                        "cold_call_ms_median": r["cold_call_ms_median"],

@@ -10,7 +10,8 @@
  * computed as the Winograd F(m x m, 3 x 3) transformed convolution of Eq. 3,
  * y = A^T [ sum_c (G w G^T) (.) (B^T d B) ] A over overlap-add tiles of edge
  * T = m + 2 (Sec. 2.1), for m in {2, 4, 5, 6} (m = 5, T = 7, is the tile of the
- * paper's experiments, Sec. 6).
+ * paper's experiments, Sec. 6), or as the FFT-tile convolution of the same
+ * sections with T = 16 (m = 14; Sec. 4 gives T >= 16 for FFT).
  *
  * Layouts: x is N x C x H x W, w is K x C x 3 x 3, y is N x K x H x W, all dense
  * row-major fp32.  x, w and y are device pointers on the plan's device.
@@ -24,7 +25,14 @@
  *   WINO_ALGO_THREE_STAGE the standard pipeline of Sec. 3: all input transforms
  *                         to device memory, T^2 products over C, then all output
  *                         transforms.
- * Both first transform the kernels (Sec. 3, step 2: kernel matrices obtained by
+ *   WINO_ALGO_FFT         fused like WINO_ALGO_FUSED, with the 16 x 16 discrete
+ *                         Fourier transform in place of the Winograd transforms
+ *                         (m must be 14): per tile the 16 x 9 frequencies of the
+ *                         half spectrum (the rest are complex conjugates,
+ *                         Sec. 2.1), complex products over C against the
+ *                         conjugated spectra of the zero-padded kernels (the
+ *                         convolution theorem for the correlation above).
+ * All first transform the kernels (Sec. 3, step 2: kernel matrices obtained by
  * transforming the kernels), unless the weights were set ahead of time with
  * wino_conv_set_weights.
  *
@@ -55,7 +63,8 @@ enum {
 
 enum {
     WINO_ALGO_FUSED = 0,
-    WINO_ALGO_THREE_STAGE = 1
+    WINO_ALGO_THREE_STAGE = 1,
+    WINO_ALGO_FFT = 2
 };
 
 /* Intermediate buffers a plan owns (for wino_conv_copy_intermediate). */
@@ -115,14 +124,19 @@ typedef struct {
  * transformed kernels (T^2 * C * K floats rounded up to the blocking) and, when
  * the last round of work items is split across compute units, their partial
  * outputs and arrival counters (zeroed here; every call leaves them zero).
- * Returns NULL (see wino_last_error) if a size is < 1, m is not 2, 4, 5 or 6, a
+ * Returns NULL (see wino_last_error) if a size is < 1, m is not 2, 4, 5 or 6 (14
+ * for WINO_ALGO_FFT, which takes no other m), a
  * size overflows the 32-bit offsets the kernels use (each of x and y must be
  * below 2^31 bytes), or the allocation fails. */
 wino_plan *wino_conv_plan(int N, int C, int K, int H, int W, int m);
 
 /* As wino_conv_plan, choosing the algorithm (WINO_ALGO_*) and optional blocking
- * overrides (t may be NULL).  The three-stage plan also allocates its
- * intermediate buffers (2 * T^2 * tiles * max(C, K) floats, rounded up). */
+ * overrides (t may be NULL; they apply to WINO_ALGO_FUSED and are ignored by the
+ * others, except that channel_splits > 1 is refused for them).  The
+ * three-stage plan also allocates its intermediate buffers (2 * T^2 * tiles *
+ * max(C, K) floats, rounded up); the FFT plan's transformed kernels take
+ * 144 * 16 bytes per (input, output) channel pair, padded to multiples of 4 and
+ * 16. */
 wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
                              const wino_tuning *t);
 
@@ -151,8 +165,10 @@ void wino_conv_destroy(wino_plan *p);
 size_t wino_conv_workspace_bytes(const wino_plan *p);
 
 /* Sizes of the problem: number of tiles N*ceil(H/m)*ceil(W/m), direct-convolution
- * flops 2*N*C*K*H*W*9 and transform-domain flops 2*T^2*tiles*C*K.  Any output
- * pointer may be NULL.  Returns WINO_EINVAL for a NULL plan. */
+ * flops 2*N*C*K*H*W*9 and transform-domain flops 2*T^2*tiles*C*K (FFT:
+ * 8*144*tiles*C*K, four real multiply-adds per complex one at each of the 144
+ * kept frequencies).  Any output pointer may be NULL.  Returns WINO_EINVAL for
+ * a NULL plan. */
 int wino_conv_info(const wino_plan *p, long long *n_tiles, double *direct_flops,
                    double *tdomain_flops);
 
@@ -163,6 +179,11 @@ int wino_conv_info(const wino_plan *p, long long *n_tiles, double *direct_flops,
  *                     (c%4)*16 + k%16, slot f%4 (the matrix-core operand order);
  *                     slots past f = T^2 - 1 (F(5)) hold zeros.  Dims returned:
  *                     {Kb, Cs, 4*Q, 64} with f in the third dim as described.
+ *                     FFT plans: [Cs][Kb][144][64][4], element (f, c, k) at cs =
+ *                     c/4, kb = k/16, frequency f = p*9 + q (spectrum row p,
+ *                     column q <= 8), lane (c%4)*16 + k%16, holding {Re, Im,
+ *                     -Im, 0} of the spectrum of w[k,c] zero-padded to 16 x 16;
+ *                     dims returned {Cs, Kb, 144, 256}.
  *   WINO_BUF_INPUT:   [T^2][Cp][tiles_p]  (three-stage plans only)
  *   WINO_BUF_PRODUCT: [T^2][Kp][tiles_p]  (three-stage plans only)
  * Frequency f = i*T + j for transform row i, column j; tile t = (n*TH + ty)*TW + tx. */

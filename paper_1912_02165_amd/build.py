@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libwino_conv.so")
 SOURCES = [os.path.join(CSRC, "wino_kernels.hip"), os.path.join(CSRC, "wino_api.cpp"),
-           os.path.join(CSRC, "wino_tune.cpp")]
+           os.path.join(CSRC, "wino_tune.cpp"), os.path.join(CSRC, "fft_kernels.hip")]
 ARCH = "gfx950"
 
 

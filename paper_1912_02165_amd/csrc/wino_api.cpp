@@ -54,12 +54,19 @@ int hip_fail(const char *what, hipError_t e) {
 }
 
 // 64-bit geometry with overflow checks; fills g on success.
-int make_geometry(int N, int C, int K, int H, int W, int m, Geometry *g) {
+// Tiles of edge T = m + 2 (Winograd) or T = 16, m = 14 (FFT, whose T2 counts
+// the 16 x 9 kept frequencies of a tile's half spectrum).
+int make_geometry(int N, int C, int K, int H, int W, int m, int algo, Geometry *g) {
     if (N < 1 || C < 1 || K < 1 || H < 1 || W < 1) {
         set_err("sizes must be >= 1 (N=%d C=%d K=%d H=%d W=%d)", N, C, K, H, W);
         return WINO_EINVAL;
     }
-    if (m != 2 && m != 4 && m != 5 && m != 6) {
+    if (algo == WINO_ALGO_FFT) {
+        if (m != 14) {
+            set_err("m=%d: the FFT algorithm uses 16 x 16 tiles, m = 14", m);
+            return WINO_EINVAL;
+        }
+    } else if (m != 2 && m != 4 && m != 5 && m != 6) {
         set_err("m=%d: only F(2x2,3x3), F(4x4,3x3), F(5x5,3x3) and F(6x6,3x3) are supported", m);
         return WINO_EINVAL;
     }
@@ -73,7 +80,7 @@ int make_geometry(int N, int C, int K, int H, int W, int m, Geometry *g) {
     }
     g->N = N; g->C = C; g->K = K; g->H = H; g->W = W; g->m = m;
     g->T = (int)T;
-    g->T2 = (int)(T * T);
+    g->T2 = algo == WINO_ALGO_FFT ? (int)(T * (T / 2 + 1)) : (int)(T * T);
     g->TH = (int)TH;
     g->TW = (int)TW;
     g->ntiles = (int)ntiles;
@@ -162,6 +169,9 @@ int run_body(const wino_plan *p, const float *x, float *y, hipStream_t s) {
     if (p->algo == WINO_ALGO_FUSED) {
         e = wino::launch_fused(p->g, p->fcfg, x, p->wt, y, p->split, s);
         if (e != hipSuccess) return hip_fail("fused kernel launch", e);
+    } else if (p->algo == WINO_ALGO_FFT) {
+        e = wino::launch_fft_fused(p->g, x, p->wt, y, s);
+        if (e != hipSuccess) return hip_fail("FFT kernel launch", e);
     } else {
         e = wino::launch_input_transform(p->g, x, p->U, s);
         if (e != hipSuccess) return hip_fail("input transform launch", e);
@@ -204,11 +214,11 @@ const char *wino_last_error(void) { return g_err.c_str(); }
 wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
                              const wino_tuning *t) {
     Geometry g;
-    if (make_geometry(N, C, K, H, W, m, &g) != WINO_OK) return nullptr;
-    if (algo != WINO_ALGO_FUSED && algo != WINO_ALGO_THREE_STAGE) {
+    if (algo != WINO_ALGO_FUSED && algo != WINO_ALGO_THREE_STAGE && algo != WINO_ALGO_FFT) {
         set_err("unknown algorithm %d", algo);
         return nullptr;
     }
+    if (make_geometry(N, C, K, H, W, m, algo, &g) != WINO_OK) return nullptr;
     FusedCfg cfg = wino::fused_cfg_default(g);
     if (t) {
         if (t->schedule < 0 || t->k_blocks_per_wave < 0 || t->waves_per_group < 0 ||
@@ -239,8 +249,11 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
                 cfg.schedule, cfg.nkb, cfg.waves, cfg.tb, m);
         return nullptr;
     }
-    // frequencies in float4 groups, the last one padded when T^2 is odd (F(5))
-    const size_t wt_bytes = (size_t)g.Kb_alloc * 16 * g.Cs * 4 * ((g.T2 + 3) / 4 * 4) * sizeof(float);
+    // frequencies in float4 groups, the last one padded when T^2 is odd (F(5));
+    // FFT: a float4 {Re, Im, -Im, 0} per frequency
+    const size_t wt_bytes = algo == WINO_ALGO_FFT
+                                ? (size_t)g.Cs * 4 * g.Kb * 16 * g.T2 * 4 * sizeof(float)
+                                : (size_t)g.Kb_alloc * 16 * g.Cs * 4 * ((g.T2 + 3) / 4 * 4) * sizeof(float);
     size_t U_bytes = 0, M_bytes = 0;
     if (algo == WINO_ALGO_THREE_STAGE) {
         U_bytes = (size_t)g.T2 * g.Cs * 4 * g.tiles_p * sizeof(float);
@@ -313,7 +326,8 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         fprintf(stderr,
                 "[wino] plan N=%d C=%d K=%d H=%d W=%d m=%d algo=%s tiles=%d schedule=%d tb=%d "
                 "nkb=%d waves=%d channel_splits=%d workspace=%zu B\n",
-                N, C, K, H, W, m, algo == WINO_ALGO_FUSED ? "fused" : "three_stage", g.ntiles,
+                N, C, K, H, W, m,
+                algo == WINO_ALGO_FUSED ? "fused" : algo == WINO_ALGO_FFT ? "fft" : "three_stage", g.ntiles,
                 cfg.schedule, cfg.tb, cfg.nkb, cfg.waves, cfg.csplit, total_bytes);
     return p;
 oom:
@@ -361,7 +375,9 @@ int wino_conv_info(const wino_plan *p, long long *n_tiles, double *direct_flops,
     const Geometry &g = p->g;
     if (n_tiles) *n_tiles = g.ntiles;
     if (direct_flops) *direct_flops = 2.0 * g.N * g.C * g.K * g.H * g.W * 9.0;
-    if (tdomain_flops) *tdomain_flops = 2.0 * g.T2 * (double)g.ntiles * g.C * g.K;
+    // FFT: T2 complex frequencies, four real multiply-adds per complex one
+    const double per = p->algo == WINO_ALGO_FFT ? 8.0 * g.T2 : 2.0 * g.T2;
+    if (tdomain_flops) *tdomain_flops = per * (double)g.ntiles * g.C * g.K;
     return WINO_OK;
 }
 
@@ -378,7 +394,8 @@ int wino_conv_run(const wino_plan *p, const float *x, const float *w, float *y, 
         set_err("y overlaps w");
         return WINO_EINVAL;
     }
-    hipError_t e = wino::launch_weight_transform(p->g, w, p->wt, s);
+    hipError_t e = p->algo == WINO_ALGO_FFT ? wino::launch_fft_weight_transform(p->g, w, p->wt, s)
+                                            : wino::launch_weight_transform(p->g, w, p->wt, s);
     if (e != hipSuccess) return hip_fail("kernel transform launch", e);
     p->weights_set = true;  // wt now holds this call's kernels
     return run_body(p, x, y, s);
@@ -393,7 +410,8 @@ int wino_conv_set_weights(wino_plan *p, const float *w, void *stream) {
     int rc;
     if ((rc = check_stream(p, s)) != WINO_OK) return rc;
     if ((rc = check_device_ptr(w, w_bytes(p->g), p->device, "w")) != WINO_OK) return rc;
-    hipError_t e = wino::launch_weight_transform(p->g, w, p->wt, s);
+    hipError_t e = p->algo == WINO_ALGO_FFT ? wino::launch_fft_weight_transform(p->g, w, p->wt, s)
+                                            : wino::launch_weight_transform(p->g, w, p->wt, s);
     if (e != hipSuccess) return hip_fail("kernel transform launch", e);
     p->weights_set = true;
     return WINO_OK;
@@ -422,6 +440,10 @@ int wino_conv_intermediate_dims(const wino_plan *p, int which, long long dims[4]
     const Geometry &g = p->g;
     switch (which) {
         case WINO_BUF_WEIGHTS:
+            if (p->algo == WINO_ALGO_FFT) {
+                dims[0] = g.Cs; dims[1] = g.Kb; dims[2] = g.T2; dims[3] = 256;
+                return WINO_OK;
+            }
             dims[0] = g.Kb_alloc; dims[1] = g.Cs; dims[2] = (g.T2 + 3) / 4 * 4; dims[3] = 64;
             return WINO_OK;
         case WINO_BUF_INPUT:

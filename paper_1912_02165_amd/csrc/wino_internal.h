@@ -11,7 +11,7 @@ namespace wino {
 // Problem geometry and device buffers of one plan.
 struct Geometry {
     int N, C, K, H, W, m;
-    int T, T2;          // input tile edge m + 2 and frequencies T^2
+    int T, T2;          // input tile edge m + 2 and frequencies T^2 (FFT: 16 and 16 * 9)
     int TH, TW;         // tiles per column / row: ceil(H/m), ceil(W/m)
     int ntiles;         // N * TH * TW
     int Cs;             // channel steps of 4 (matrix-core reduction depth): ceil(C/4)
@@ -63,6 +63,10 @@ hipError_t launch_input_transform(const Geometry &g, const float *x, float *U, h
 hipError_t launch_frequency_gemm(const Geometry &g, const float *U, const float *wt, float *M,
                                  hipStream_t s);
 hipError_t launch_output_transform(const Geometry &g, const float *M, float *y, hipStream_t s);
+
+// FFT-tile algorithm (16 x 16 tiles, m = 14): kernel spectra, then the fused kernel.
+hipError_t launch_fft_weight_transform(const Geometry &g, const float *w, float *wt, hipStream_t s);
+hipError_t launch_fft_fused(const Geometry &g, const float *x, const float *wt, float *y, hipStream_t s);
 
 // Sets the message wino_last_error() returns on the calling thread (printf format).
 void set_error(const char *fmt, ...);

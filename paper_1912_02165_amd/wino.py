@@ -14,10 +14,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libwino_conv.so")
 
 WINO_OK, WINO_EINVAL, WINO_EUNSUPPORTED, WINO_ENOMEM, WINO_EHIP = 0, -1, -2, -3, -4
-WINO_ALGO_FUSED, WINO_ALGO_THREE_STAGE = 0, 1
+WINO_ALGO_FUSED, WINO_ALGO_THREE_STAGE, WINO_ALGO_FFT = 0, 1, 2
 WINO_BUF_WEIGHTS, WINO_BUF_INPUT, WINO_BUF_PRODUCT = 0, 1, 2
 
-ALGOS = {"fused": WINO_ALGO_FUSED, "three_stage": WINO_ALGO_THREE_STAGE}
+ALGOS = {"fused": WINO_ALGO_FUSED, "three_stage": WINO_ALGO_THREE_STAGE, "fft": WINO_ALGO_FFT}
+ALGO_NAMES = {v: k for k, v in ALGOS.items()}
 
 # Every symbol the header declares, with (restype, argtypes).
 _vp = ctypes.c_void_p
@@ -246,7 +247,7 @@ class Plan:
         """The fastest plan among the candidates (timed now, or from the wisdom table);
         its m, algorithm and measured call time are attributes."""
         h, m, algo, us = wino_conv_plan_tuned(N, C, K, H, W, candidates)
-        p = cls(N, C, K, H, W, m, "fused" if algo == WINO_ALGO_FUSED else "three_stage", _handle=h)
+        p = cls(N, C, K, H, W, m, ALGO_NAMES[algo], _handle=h)
         p.call_us = us
         return p
 

@@ -5,13 +5,18 @@ element error normalised by the largest reference magnitude):
     F(2x2,3x3): rel_l2 <= 1e-5;  F(4x4,3x3), F(6x6,3x3): rel_l2 <= 1e-4;
     F(5x5,3x3) (not among the stated tolerances; its tile lies between F(4) and
     F(6), so it takes theirs): rel_l2 <= 1e-4;
+    FFT tiles (16 x 16, m = 14; not among the stated tolerances): rel_l2 <= 1e-5.
+    The error of an fp32 radix-2 FFT grows with the number of butterfly levels,
+    about eps * log2(n) relative: 8 levels forward and 8 inverse on 16 x 16
+    tiles give ~1e-6 (eps = 6e-8), a tenth of the bound, to which the products
+    add the usual fp32 sum over 9C terms;
     all: max|y - y_ref| / max|y_ref| <= 1e-3.
 The reference is the fp64 oracle; the GPU computes in fp32.
 """
 
 import numpy as np
 
-REL_L2 = {2: 1e-5, 4: 1e-4, 5: 1e-4, 6: 1e-4}
+REL_L2 = {2: 1e-5, 4: 1e-4, 5: 1e-4, 6: 1e-4, 14: 1e-5}
 MAX_ERR = 1e-3
 
 

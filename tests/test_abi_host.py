@@ -67,6 +67,29 @@ def test_bad_m(lib, m):
     assert "only F(2x2" in _plan_fails(lib, 1, 4, 4, 8, 8, m, wino.WINO_ALGO_FUSED, None)
 
 
+@pytest.mark.parametrize("m", [2, 4, 6, 13, 16])
+def test_fft_needs_m14(lib, m):
+    assert "m = 14" in _plan_fails(lib, 1, 4, 4, 8, 8, m, wino.WINO_ALGO_FFT, None)
+
+
+def test_m14_is_fft_only(lib):
+    for algo in (wino.WINO_ALGO_FUSED, wino.WINO_ALGO_THREE_STAGE):
+        assert "only F(2x2" in _plan_fails(lib, 1, 4, 4, 8, 8, 14, algo, None)
+
+
+def test_fft_refuses_channel_splits(lib):
+    t = wino.WinoTuning(channel_splits=2)
+    assert "specialised" in _plan_fails(lib, 1, 8, 4, 8, 8, 14, wino.WINO_ALGO_FFT, ctypes.byref(t))
+
+
+def test_algorithm_names():
+    assert wino.ALGOS == {"fused": 0, "three_stage": 1, "fft": 2}
+    with open(os.path.join(ROOT, "include", "wino_conv.h")) as f:
+        hdr = f.read()
+    for name, value in (("WINO_ALGO_FUSED", 0), ("WINO_ALGO_THREE_STAGE", 1), ("WINO_ALGO_FFT", 2)):
+        assert re.search(r"%s = %d\b" % (name, value), hdr)
+
+
 def test_f5_only_specialised(lib):
     """F(5) is built for the warp-specialised fused kernel only."""
     t = wino.WinoTuning(schedule=wino.WINO_SCHED_SHARED)
