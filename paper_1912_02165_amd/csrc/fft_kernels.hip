@@ -29,6 +29,26 @@ namespace wino {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef int int32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer loads: an offset at or past the resource's size reads 0, which
+// gives the zero padding of input windows without branches.
+__device__ float fft_buffer_load_f32(int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.load.f32");
+__device__ void fft_buffer_store_f32(float v, int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.store.f32");
+__device__ __forceinline__ int32x4 fft_rsrc(const float *base, unsigned bytes) {
+    const unsigned long long p = reinterpret_cast<unsigned long long>(base);
+    int32x4 r;
+    r[0] = (int)(unsigned)(p & 0xffffffffull);
+    r[1] = (int)(unsigned)((p >> 32) & 0xffffull);  // stride 0
+    r[2] = (int)bytes;                                 // range-checked size
+    r[3] = 0x00020000;                                 // 32-bit data format
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = __builtin_amdgcn_readfirstlane(r[i]);
+    return r;
+}
+constexpr unsigned kFOutside = 0x80000000u;  // past every buffer (each is below 2^31 bytes)
 
 constexpr int kFT = 16;             // tile edge
 constexpr int kFM = 14;             // output tile edge
@@ -161,6 +181,17 @@ __global__ void __launch_bounds__(256) fft_weight_transform_kernel(const float *
     }
 }
 
+// Row transforms of two real rows at once: z = a + i b has spectrum Z, and
+// A[q] = (Z[q] + conj Z[-q]) / 2, B[q] = (Z[q] - conj Z[-q]) / 2i.
+__device__ __forceinline__ void unpack_real_pair(const float (&zr)[16], const float (&zi)[16], int q,
+                                                 float &ar, float &ai, float &br, float &bi) {
+    const int qc = (16 - q) & 15;
+    ar = 0.5f * (zr[q] + zr[qc]);
+    ai = 0.5f * (zi[q] - zi[qc]);
+    br = 0.5f * (zi[q] + zi[qc]);
+    bi = 0.5f * (zr[qc] - zr[q]);
+}
+
 __global__ void __launch_bounds__(512) fft_fused_kernel(const float *__restrict__ x,
                                                          const floatx4 *__restrict__ wt,
                                                          float *__restrict__ y, Geometry g) {
@@ -173,16 +204,28 @@ __global__ void __launch_bounds__(512) fft_fused_kernel(const float *__restrict_
     constexpr int kXR = 17, kXT = 273;
     __shared__ float xin[64 * kXT];
     __shared__ float spec[kFF * 2 * 64];
-    __shared__ int tinfo[16][3];  // per tile of the item: image (-1: no tile), first row, first column
+    // per tile of the item: x offset of its window's first element in channel 0
+    // (may be negative: the window starts one row and column before the tile),
+    // the rows (bits 0-15) and columns (bits 16-31) of the window inside the
+    // image (0: no tile), the image, and the first output row and column
+    __shared__ int tbase[16], tmask[16], tn[16], toy[16], tox[16];
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int tg = blockIdx.x / g.Kb, kb = blockIdx.x - tg * g.Kb;
     const long long HW = (long long)g.H * g.W;
     if (tid < 16) {
         const FTile ft = fft_tile(g, tg * 16 + tid);
-        tinfo[tid][0] = ft.ok ? ft.n : -1;
-        tinfo[tid][1] = ft.ty * kFM - 1;
-        tinfo[tid][2] = ft.tx * kFM - 1;
+        const int oy = ft.ty * kFM, ox = ft.tx * kFM;
+        unsigned rows = 0, cols = 0;
+        for (int e = 0; e < kFT; ++e) {
+            if (oy - 1 + e >= 0 && oy - 1 + e < g.H) rows |= 1u << e;
+            if (ox - 1 + e >= 0 && ox - 1 + e < g.W) cols |= 1u << e;
+        }
+        tbase[tid] = (int)((long long)ft.n * g.C * HW + (long long)(oy - 1) * g.W + (ox - 1));
+        tmask[tid] = ft.ok ? (int)(rows | (cols << 16)) : 0;
+        tn[tid] = ft.ok ? ft.n : -1;
+        toy[tid] = oy;
+        tox[tid] = ox;
     }
 
     floatx4 acc_re[kFPerWave], acc_im[kFPerWave];
@@ -194,40 +237,62 @@ __global__ void __launch_bounds__(512) fft_fused_kernel(const float *__restrict_
     const floatx4 *wk = wt + (long long)kb * kFF * 64 + lane;  // + cs * Kb * 144 * 64
     __syncthreads();
 
-    for (int cs = 0; cs < g.Cs; ++cs) {
-        // 1. input tiles, zero outside the image and past the last channel:
-        //    element e = tid + 512 s is tile-channel e >> 8, row (e >> 4) & 15,
-        //    column e & 15 (16 consecutive threads read one tile row)
-#pragma unroll 4
+    // Input element s (0..31) of this thread in a stage: tile-channel tc =
+    // (tid >> 8) + 2 s (channel s >> 3, tile (tid >> 8) + 2 (s & 7)), window row
+    // ei = (tid >> 4) & 15, column ej = tid & 15; 16 consecutive threads read one
+    // window row.
+    const int eh = tid >> 8, ei = (tid >> 4) & 15, ej = tid & 15;
+    const int erel = ei * g.W + ej;
+    const int32x4 xrs = fft_rsrc(x, (unsigned)((long long)g.N * g.C * HW * 4));
+    const int32x4 yrs = fft_rsrc(y, (unsigned)((long long)g.N * g.K * HW * 4));
+    float xr[32];
+    auto load_stage = [&](int cs) {
+#pragma unroll
         for (int s = 0; s < 32; ++s) {
-            const int e = tid + 512 * s;
-            const int tc = e >> 8, i = (e >> 4) & 15, j = e & 15;
-            const int t = tc & 15, ch = cs * 4 + (tc >> 4);
-            const int n = tinfo[t][0];
-            const int iy = tinfo[t][1] + i, ix = tinfo[t][2] + j;
-            float v = 0.0f;
-            if (n >= 0 && ch < g.C && iy >= 0 && iy < g.H && ix >= 0 && ix < g.W)
-                v = x[((long long)n * g.C + ch) * HW + (long long)iy * g.W + ix];
-            xin[tc * kXT + i * kXR + j] = v;
+            const int t = eh + 2 * (s & 7), ch = cs * 4 + (s >> 3);
+            const unsigned msk = (unsigned)tmask[t];
+            const bool in = ((msk >> ei) & (msk >> (16 + ej)) & 1u) && ch < g.C;
+            // outside the window's valid part the offset gets the top bit (past the
+            // buffer), without a branch around the load
+            // (unsigned arithmetic: the unused offsets of padding channels may wrap)
+            const unsigned el = (unsigned)tbase[t] + (unsigned)ch * (unsigned)HW + (unsigned)erel;
+            const unsigned off = (el * 4u & ~kFOutside) | (in ? 0u : kFOutside);
+            xr[s] = fft_buffer_load_f32(xrs, off, 0, 0);
         }
+    };
+    load_stage(0);
+
+    for (int cs = 0; cs < g.Cs; ++cs) {
+        // 1. the stage's input tiles (loaded during the previous stage's products)
+#pragma unroll
+        for (int s = 0; s < 32; ++s) xin[(eh + 2 * s) * kXT + ei * kXR + ej] = xr[s];
         __syncthreads();
-        // 2. along rows: 1024 rows (tile-channel r & 63, row r >> 6), two per thread;
-        //    row i's 9 kept values go to spec at frequency i * 9 + q for now
-#pragma unroll 1
-        for (int h = 0; h < 2; ++h) {
-            const int r = tid + 512 * h;
-            const int tc = r & 63, i = r >> 6;
+        // kernel operands of the first frequencies, in flight during the transforms
+        const floatx4 *ws = wk + (long long)cs * g.Kb * kFF * 64 + wave * kFPerWave * 64;
+        constexpr int kCh = 3;  // frequencies per operand chunk
+        floatx4 a0[kCh];
+#pragma unroll
+        for (int j = 0; j < kCh; ++j) a0[j] = ws[j * 64];
+        // 2. along rows: rows i and i + 8 of tile-channel tc (= tid & 63, i = tid >> 6)
+        //    as one complex transform; row i's 9 kept values go to spec at
+        //    frequency i * 9 + q for now
+        {
+            const int tc = tid & 63, i = tid >> 6;
             float re[16], im[16];
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
                 re[j] = xin[tc * kXT + i * kXR + j];
-                im[j] = 0.0f;
+                im[j] = xin[tc * kXT + (i + 8) * kXR + j];
             }
             dft16<-1>(re, im);
 #pragma unroll
             for (int q = 0; q < kFQ; ++q) {
-                spec[((i * kFQ + q) * 2 + 0) * 64 + tc] = re[q];
-                spec[((i * kFQ + q) * 2 + 1) * 64 + tc] = im[q];
+                float ar, ai, br, bi;
+                unpack_real_pair(re, im, q, ar, ai, br, bi);
+                spec[((i * kFQ + q) * 2 + 0) * 64 + tc] = ar;
+                spec[((i * kFQ + q) * 2 + 1) * 64 + tc] = ai;
+                spec[(((i + 8) * kFQ + q) * 2 + 0) * 64 + tc] = br;
+                spec[(((i + 8) * kFQ + q) * 2 + 1) * 64 + tc] = bi;
             }
         }
         __syncthreads();
@@ -250,24 +315,29 @@ __global__ void __launch_bounds__(512) fft_fused_kernel(const float *__restrict_
             }
         }
         __syncthreads();
+        // next stage's input tiles, in flight during the products
+        if (cs + 1 < g.Cs) load_stage(cs + 1);
         // 4. products of the wave's frequencies: lane = channel-in-stage * 16 +
         //    tile reads operand B; its kernel operands {Wr, Wi, -Wi} come as one
-        //    float4
-        const floatx4 *ws = wk + (long long)cs * g.Kb * kFF * 64;
+        //    float4, the next chunk's loaded while one is multiplied
+        floatx4 a1[kCh];
 #pragma unroll
-        for (int j0 = 0; j0 < kFPerWave; j0 += 6) {
-            floatx4 a[6];
+        for (int j0 = 0; j0 < kFPerWave; j0 += kCh) {
+            if (j0 + kCh < kFPerWave) {
 #pragma unroll
-            for (int j = 0; j < 6; ++j) a[j] = ws[(wave * kFPerWave + j0 + j) * 64];
+                for (int j = 0; j < kCh; ++j) a1[j] = ws[(j0 + kCh + j) * 64];
+            }
 #pragma unroll
-            for (int j = 0; j < 6; ++j) {
+            for (int j = 0; j < kCh; ++j) {
                 const int f = wave * kFPerWave + j0 + j;
                 const float br = spec[(f * 2 + 0) * 64 + lane], bi = spec[(f * 2 + 1) * 64 + lane];
-                acc_re[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j].x, br, acc_re[j0 + j], 0, 0, 0);
-                acc_re[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j].y, bi, acc_re[j0 + j], 0, 0, 0);
-                acc_im[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j].x, bi, acc_im[j0 + j], 0, 0, 0);
-                acc_im[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j].z, br, acc_im[j0 + j], 0, 0, 0);
+                acc_re[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[j].x, br, acc_re[j0 + j], 0, 0, 0);
+                acc_re[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[j].y, bi, acc_re[j0 + j], 0, 0, 0);
+                acc_im[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[j].x, bi, acc_im[j0 + j], 0, 0, 0);
+                acc_im[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[j].z, br, acc_im[j0 + j], 0, 0, 0);
             }
+#pragma unroll
+            for (int j = 0; j < kCh; ++j) a0[j] = a1[j];
         }
         __syncthreads();  // xin and spec are rewritten by the next stage
     }
@@ -304,31 +374,44 @@ __global__ void __launch_bounds__(512) fft_fused_kernel(const float *__restrict_
             }
         }
         __syncthreads();
-        // inverse along rows for output rows 0..13: the dropped columns 9..15 are
-        // the conjugates of columns 7..1 (the row is real); 896 rows
-#pragma unroll 1
-        for (int r = tid; r < 64 * kFM; r += 512) {
-            const int pr = r & 63, i = r >> 6;
+        // inverse along rows for output rows i and i + 7 (i < 7) of pair pr as one
+        // complex transform: row i's spectrum (completed by conjugate symmetry,
+        // imaginary parts at q = 0 and 8 dropped as for a real row) plus i times
+        // row i + 7's gives row i in the real part, row i + 7 in the imaginary part
+        if (tid < 64 * 7) {
+            const int pr = tid & 63, i = tid >> 6;
             float re[16], im[16];
 #pragma unroll
             for (int q = 0; q < kFQ; ++q) {
-                re[q] = spec[((i * kFQ + q) * 2 + 0) * 64 + pr];
-                im[q] = spec[((i * kFQ + q) * 2 + 1) * 64 + pr];
-            }
-#pragma unroll
-            for (int q = kFQ; q < 16; ++q) {
-                re[q] = re[16 - q];
-                im[q] = -im[16 - q];
+                const float ar = spec[((i * kFQ + q) * 2 + 0) * 64 + pr];
+                const float ai = (q == 0 || q == 8) ? 0.0f : spec[((i * kFQ + q) * 2 + 1) * 64 + pr];
+                const float br = spec[(((i + 7) * kFQ + q) * 2 + 0) * 64 + pr];
+                const float bi = (q == 0 || q == 8) ? 0.0f : spec[(((i + 7) * kFQ + q) * 2 + 1) * 64 + pr];
+                re[q] = ar - bi;
+                im[q] = ai + br;
+                if (q > 0 && q < 8) {  // column 16 - q: conj(A) + i conj(B)
+                    re[16 - q] = ar + bi;
+                    im[16 - q] = br - ai;
+                }
             }
             dft16<1>(re, im);
+            // stores outside the image (or of a missing tile or output channel)
+            // get an offset past the buffer and are dropped
             const int t = pr & 15, k = kb * 16 + 4 * (pr >> 4) + v;
-            const int n = tinfo[t][0];
-            const int oy = tinfo[t][1] + 1 + i, ox0 = tinfo[t][2] + 1;
-            if (n >= 0 && k < g.K && oy < g.H) {
-                float *yr = y + ((long long)n * g.K + k) * HW + (long long)oy * g.W + ox0;
+            const int n = tn[t], ox0 = tox[t];
+            const bool ok = n >= 0 && k < g.K;
+            // (unsigned arithmetic: offsets that are not used may wrap)
+            const unsigned kbase = ((unsigned)(ok ? n : 0) * (unsigned)g.K + (unsigned)k) * (unsigned)HW;
 #pragma unroll
-                for (int j = 0; j < kFM; ++j)
-                    if (ox0 + j < g.W) yr[j] = re[j] * kScale;
+            for (int half = 0; half < 2; ++half) {
+                const int oy = toy[t] + i + 7 * half;
+                const bool rok = ok && oy < g.H;
+                const unsigned rowoff = (kbase + (unsigned)(oy * g.W + ox0)) * 4u;
+#pragma unroll
+                for (int j = 0; j < kFM; ++j) {
+                    const unsigned off = (rok && ox0 + j < g.W) ? rowoff + 4u * j : kFOutside;
+                    fft_buffer_store_f32((half ? im[j] : re[j]) * kScale, yrs, off, 0, 0);
+                }
             }
         }
         __syncthreads();  // spec is rewritten by the next round
