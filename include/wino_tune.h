@@ -6,14 +6,16 @@
  * says that tuning is done once and stored in a wisdom file.  Here the tuned
  * parameter is the tile size m of F(m x m, 3 x 3), m in {2, 4, 5, 6} (the
  * paper's T = m + 2; the number of tiles per task is fixed by the matrix-core
- * blocking) and, optionally, the algorithm (fused or three-stage).  A tuning result is remembered per
+ * blocking) and, optionally, the algorithm (fused or three-stage at each m, or
+ * the FFT-tile algorithm with m = 14).  A tuning result is remembered per
  * (GPU architecture, compute units, N, C, K, H, W, candidate set) in a
  * process-wide wisdom table that can be written to and read from a text file.
  *
  * Wisdom file: text, one entry per line, '#' starts a comment line:
  *     <arch> <cus> <N> <C> <K> <H> <W> <candidates> <m> <algo> <microseconds>
  * arch is the device's architecture name (e.g. gfx950), candidates is the
- * candidate mask in hexadecimal (0x...), algo is 0 (fused) or 1 (three-stage)
+ * candidate mask in hexadecimal (0x...), algo is 0 (fused), 1 (three-stage) or
+ * 2 (FFT, with m = 14)
  * and microseconds the measured time of one call.
  *
  * Thread safety: the wisdom table is guarded by a lock; plans are as in
@@ -28,20 +30,21 @@
 extern "C" {
 #endif
 
-/* Candidate mask bits: tile sizes, and whether the three-stage algorithm is
- * also tried at each of them. */
+/* Candidate mask bits: tile sizes, whether the three-stage algorithm is also
+ * tried at each of them, and whether the FFT-tile algorithm is tried. */
 enum {
     WINO_TUNE_M2 = 1 << 2,
     WINO_TUNE_M4 = 1 << 4,
     WINO_TUNE_M5 = 1 << 5,
     WINO_TUNE_M6 = 1 << 6,
-    WINO_TUNE_THREE_STAGE = 1 << 8
+    WINO_TUNE_THREE_STAGE = 1 << 8,
+    WINO_TUNE_FFT = 1 << 9  /* the FFT-tile algorithm (m = 14) */
 };
 
 /* A plan for the convolution of wino_conv_plan (N x C x H x W input, K output
  * channels) with the m and algorithm that run fastest on the current device
  * among the candidates (a nonzero mask of WINO_TUNE_* bits with at least one
- * WINO_TUNE_M* bit).  If the wisdom table holds the answer it is used directly;
+ * WINO_TUNE_M* or the WINO_TUNE_FFT bit).  If the wisdom table holds the answer it is used directly;
  * otherwise every candidate is planned and timed here: its kernels transformed
  * once, then the median of 5 calls of wino_conv_run_pretransformed after 2
  * warm-up calls, on device buffers of the layer's size that this function

@@ -26,11 +26,12 @@ std::mutex g_mu;
 std::map<Key, Choice> g_table;
 
 constexpr unsigned kMBits = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M5 | WINO_TUNE_M6;
-constexpr unsigned kAllBits = kMBits | WINO_TUNE_THREE_STAGE;
+constexpr unsigned kAllBits = kMBits | WINO_TUNE_THREE_STAGE | WINO_TUNE_FFT;
 
-bool mask_ok(unsigned c) { return (c & ~kAllBits) == 0 && (c & kMBits) != 0; }
+bool mask_ok(unsigned c) { return (c & ~kAllBits) == 0 && (c & (kMBits | WINO_TUNE_FFT)) != 0; }
 
 bool choice_ok(unsigned c, int m, int algo) {
+    if (algo == WINO_ALGO_FFT) return m == 14 && (c & WINO_TUNE_FFT) != 0;
     if (m != 2 && m != 4 && m != 5 && m != 6) return false;
     if (!(c & (1u << m))) return false;
     if (algo == WINO_ALGO_THREE_STAGE) return (c & WINO_TUNE_THREE_STAGE) != 0;
@@ -121,7 +122,8 @@ wino_plan *wino_conv_plan_tuned(int N, int C, int K, int H, int W, unsigned cand
         return nullptr;
     }
     if (!mask_ok(candidates)) {
-        wino::set_error("candidate mask 0x%x: needs a WINO_TUNE_M* bit and no other bits", candidates);
+        wino::set_error("candidate mask 0x%x: needs a WINO_TUNE_M* or WINO_TUNE_FFT bit and no other bits",
+                        candidates);
         return nullptr;
     }
     std::string arch;
@@ -137,9 +139,10 @@ wino_plan *wino_conv_plan_tuned(int N, int C, int K, int H, int W, unsigned cand
     if (best.m == 0) {
         Buffers b;
         bool have_buffers = false;
-        for (int m : {2, 4, 5, 6}) {
-            if (!(candidates & (1u << m))) continue;
-            for (int algo : {WINO_ALGO_FUSED, WINO_ALGO_THREE_STAGE}) {
+        for (int m : {2, 4, 5, 6, 14}) {
+            if (m == 14 ? !(candidates & WINO_TUNE_FFT) : !(candidates & (1u << m))) continue;
+            for (int algo : {WINO_ALGO_FUSED, WINO_ALGO_THREE_STAGE, WINO_ALGO_FFT}) {
+                if ((algo == WINO_ALGO_FFT) != (m == 14)) continue;
                 if (algo == WINO_ALGO_THREE_STAGE && !(candidates & WINO_TUNE_THREE_STAGE)) continue;
                 wino_plan *p = wino_conv_plan_ex(N, C, K, H, W, m, algo, nullptr);
                 if (!p) return nullptr;  // message set by the constructor

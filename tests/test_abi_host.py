@@ -167,6 +167,7 @@ def test_python_errors_raise(lib):
 WISDOM = """# winograd wisdom: arch cus N C K H W candidates m algo microseconds
 gfx950 256 32 64 64 224 224 0x54 4 0 417.900
 gfx950 256 64 512 512 14 14 0x154 6 1 12.500
+gfx950 256 64 128 128 28 28 0x210 14 2 321.000
 """
 
 
@@ -176,8 +177,9 @@ def test_wisdom_roundtrip(lib, tmp_path):
     src = tmp_path / "in.txt"
     src.write_text(WISDOM)
     wc.wino_wisdom_load(str(src))
-    assert wc.wino_wisdom_size() == 2
+    assert wc.wino_wisdom_size() == 3
     assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (4, 0)
+    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 128, 128, 28, 28, 0x210) == (14, 2)
     assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1)
     # every key field matters
     assert wc.wino_wisdom_lookup("gfx942", 256, 32, 64, 64, 224, 224, 0x54) is None
@@ -187,7 +189,7 @@ def test_wisdom_roundtrip(lib, tmp_path):
     wc.wino_wisdom_save(str(out))
     wc.wino_wisdom_clear()
     wc.wino_wisdom_load(str(out))
-    assert wc.wino_wisdom_size() == 2
+    assert wc.wino_wisdom_size() == 3
     assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1)
     lines = [l for l in out.read_text().splitlines() if not l.startswith("#")]
     assert sorted(lines) == sorted(l for l in WISDOM.splitlines() if not l.startswith("#"))
@@ -195,7 +197,7 @@ def test_wisdom_roundtrip(lib, tmp_path):
     upd = tmp_path / "upd.txt"
     upd.write_text("gfx950 256 32 64 64 224 224 0x54 2 0 500\n")
     wc.wino_wisdom_load(str(upd))
-    assert wc.wino_wisdom_size() == 2
+    assert wc.wino_wisdom_size() == 3
     assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (2, 0)
     wc.wino_wisdom_clear()
 
@@ -207,6 +209,9 @@ def test_wisdom_roundtrip(lib, tmp_path):
     "gfx950 256 32 64 64 224 224 0x14 6 0 1.0",         # m not among the candidates
     "gfx950 256 32 64 64 224 224 0x54 4 1 1.0",         # three-stage not a candidate
     "gfx950 256 32 64 64 224 224 0x2 2 0 1.0",          # mask without a tile-size bit
+    "gfx950 256 32 64 64 224 224 0x10 14 2 1.0",        # FFT not a candidate
+    "gfx950 256 32 64 64 224 224 0x210 4 2 1.0",        # FFT with m other than 14
+    "gfx950 256 32 64 64 224 224 0x210 14 0 1.0",       # m = 14 is FFT only
     "gfx950 256 32 0 64 224 224 0x54 4 0 1.0",          # size < 1
     "gfx950 256 32 64 64 224 224 0x54 4 0 -1",          # negative time
 ])
@@ -219,7 +224,7 @@ def test_wisdom_rejects_malformed_and_keeps_table(lib, tmp_path, line):
     bad.write_text("gfx950 256 1 1 1 1 1 0x4 2 0 1.0\n" + line + "\n")
     with pytest.raises(wc.WinoError, match=r"bad.txt:2: malformed"):
         wc.wino_wisdom_load(str(bad))
-    assert wc.wino_wisdom_size() == 2          # nothing of the bad file was merged
+    assert wc.wino_wisdom_size() == 3          # nothing of the bad file was merged
     assert wc.wino_wisdom_lookup("gfx950", 256, 1, 1, 1, 1, 1, 0x4) is None
     wc.wino_wisdom_clear()
 
@@ -231,7 +236,7 @@ def test_wisdom_file_errors(lib, tmp_path):
         wc.wino_wisdom_save(str(tmp_path / "no_such_dir" / "w.txt"))
 
 
-@pytest.mark.parametrize("mask", [0, wc.WINO_TUNE_THREE_STAGE, 1 << 3, wc.WINO_TUNE_M4 | (1 << 9)])
+@pytest.mark.parametrize("mask", [0, wc.WINO_TUNE_THREE_STAGE, 1 << 3, wc.WINO_TUNE_M4 | (1 << 10)])
 def test_plan_tuned_bad_mask(lib, mask):
     assert not lib.wino_conv_plan_tuned(1, 4, 4, 8, 8, mask, None, None, None)
     assert "candidate mask" in wc.wino_last_error()

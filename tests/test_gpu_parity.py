@@ -322,7 +322,8 @@ def _device_key():
 
 
 @pytest.mark.parametrize("mask", [wc.WINO_TUNE_ALL_M | wc.WINO_TUNE_THREE_STAGE, wc.WINO_TUNE_M4,
-                                  wc.WINO_TUNE_M2 | wc.WINO_TUNE_M6])
+                                  wc.WINO_TUNE_M2 | wc.WINO_TUNE_M6, wc.WINO_TUNE_FFT,
+                                  wc.WINO_TUNE_M6 | wc.WINO_TUNE_FFT])
 def test_plan_tuned(mask, tmp_path):
     """The tuned plan is one of the candidates, matches the oracle at its m, and is
     remembered: the second request, and one after a save / clear / load of the
@@ -332,8 +333,11 @@ def test_plan_tuned(mask, tmp_path):
     print(f"\n[gpu] tuned plan mask={mask:#x}", flush=True)
     wc.wino_wisdom_clear()
     p = wc.Plan.tuned(N, C, K, H, W, mask)
-    assert mask & (1 << p.m)
-    assert p.algo == "fused" or mask & wc.WINO_TUNE_THREE_STAGE
+    if p.algo == "fft":
+        assert p.m == 14 and mask & wc.WINO_TUNE_FFT
+    else:
+        assert mask & (1 << p.m)
+        assert p.algo == "fused" or mask & wc.WINO_TUNE_THREE_STAGE
     assert wc.wino_conv_plan_params(p.handle) == (p.m, wc.ALGOS[p.algo])
     assert p.call_us > 0
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
