@@ -21,7 +21,8 @@ plus, per layer, the m and algorithm a tuned plan picks (algo "tuned"), and on
 layers with C >= 128 the fused kernel with every work item split into 2 and 4
 channel pieces (algo "fused_csplitP"); and per layer the FFT-tile algorithm
 (algo "fft", 16 x 16 tiles; its "transform-domain" rate counts the real flops
-of its complex products).
+of its complex products); and for the launch-bound 56x56 layer at F(2) one call
+captured in a HIP graph and replayed (algo "fused_graph").
 """
 
 import argparse
@@ -136,6 +137,47 @@ def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False, tuning=None):
             res["cold_call_ms_median"] = rep_times(p, x, w, y, steps, stream, scratch)
             del scratch
     return res
+
+
+def time_graph(layer, m, steps, warmup, x, w):
+    """One wino_conv_run captured in a HIP graph (torch.cuda.CUDAGraph), replayed:
+    back-to-back ms per replay and the median of separately timed replays."""
+    import torch
+    import paper_1912_02165_amd as wc
+    N, C, K, H, W = layer.N, layer.C, layer.K, layer.H, layer.W
+    y = torch.empty((N, K, H, W), dtype=torch.float32, device="cuda")
+    with wc.Plan(N, C, K, H, W, m, "fused") as p:
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for _ in range(warmup):
+                p.run(x, w, y)
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            p.run(x, w, y)
+        for _ in range(warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_step = e0.elapsed_time(e1) / steps
+        single = []
+        for _ in range(steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            g.replay()
+            b.record(stream)
+            torch.cuda.synchronize()
+            single.append(a.elapsed_time(b))
+        del g
+    return ms_step, sorted(single)[len(single) // 2]
 
 
 def cpu_baseline(layer, budget_s=20.0):
@@ -255,6 +297,14 @@ def main():
                        "weight_transform_ms": r["weight_transform_ms"]}
                 if label == "tuned":
                     row["tuned_choice"] = {"m": m_c, "algo": algo}
+                rows.append(row)
+                print(json.dumps(row), file=sys.stderr, flush=True)
+            if lay.id == 1 and mm == 2:
+                # the launch-bound layer as a replayed HIP graph of one call
+                g_step, g_single = time_graph(lay, mm, args.steps, args.warmup, xa, wa)
+                row = {"workload": lay.tag(mm), "algo": "fused_graph", "ms_per_step": g_step,
+                       "eff_tflops": lay.direct_flops / (g_step * 1e-3) / 1e12,
+                       "warm_call_ms_median": g_single}
                 rows.append(row)
                 print(json.dumps(row), file=sys.stderr, flush=True)
             del xa, wa
