@@ -46,7 +46,7 @@ enum {
  * among the candidates (a nonzero mask of WINO_TUNE_* bits with at least one
  * WINO_TUNE_M* or the WINO_TUNE_FFT bit).  If the wisdom table holds the answer it is used directly;
  * otherwise every candidate is planned and timed here: its kernels transformed
- * once, then the median of 5 calls of wino_conv_run_pretransformed after 2
+ * once, then the median of 5 calls of wino_conv_run_pretransformed after 10
  * warm-up calls, on device buffers of the layer's size that this function
  * allocates, fills with a constant and frees before returning (synchronous;
  * needs room for x, y and w beside the largest candidate's workspace).  The

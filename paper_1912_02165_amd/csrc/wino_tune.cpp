@@ -88,10 +88,11 @@ struct Buffers {
 };
 
 // Median time (microseconds) of 5 calls of the plan after its kernels are
-// transformed and 2 warm-up calls; negative status on failure.
+// transformed and 10 warm-up calls (the shader clock rises over the first
+// milliseconds of work); negative status on failure.
 int time_plan(wino_plan *p, const Buffers &b, double *us) {
     int st = wino_conv_set_weights(p, b.w, nullptr);
-    for (int i = 0; st == WINO_OK && i < 2; ++i) st = wino_conv_run_pretransformed(p, b.x, b.y, nullptr);
+    for (int i = 0; st == WINO_OK && i < 10; ++i) st = wino_conv_run_pretransformed(p, b.x, b.y, nullptr);
     std::vector<double> t;
     for (int i = 0; st == WINO_OK && i < 5; ++i) {
         hipError_t e = hipEventRecord(b.e0, nullptr);
