@@ -11,7 +11,7 @@ returned as exact ``fractions.Fraction`` matrices.  In this package's naming
 its G is ``G`` (T x 3), with T = m + 2 the input tile edge and m = T - K + 1 the
 output tile edge of the overlap-add tiling (Sec. 2.1).
 
-Construction (the reading this build takes; the paper is silent on it).  Pick
+Construction (a reading: the paper is silent on it).  Pick
 T - 1 distinct finite interpolation points p_j and the point at infinity.  The
 1D correlation y_i = sum_{u<3} g_u d_{i+u} (i < m) is the transpose of the
 polynomial product a(x) g(x) with deg a = m - 1, so with
