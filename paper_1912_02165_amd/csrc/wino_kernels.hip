@@ -151,6 +151,9 @@ __device__ void buffer_store_f32(float v, int32x4 rsrc, unsigned voffset, unsign
 // Cache-policy bit of a buffer access that makes it coherent across the device
 // (the coherence that device-scope atomic loads and stores use).
 constexpr int kDeviceCoherent = 1 << 4;
+// Cache-policy bit of a streaming (non-temporal) access: the output, written once,
+// is not kept in L2 at the expense of the transformed kernels.
+constexpr int kStream = 1 << 1;
 
 __device__ __forceinline__ int32x4 make_rsrc(const float *base, unsigned bytes) {
     const unsigned long long p = reinterpret_cast<unsigned long long>(base);
@@ -660,14 +663,14 @@ __device__ __forceinline__ void store_rows_buf(int32x4 yrs, unsigned voff, unsig
     for (int i = 0; i < M; ++i) {
         const unsigned so = soff + (unsigned)i * rowb;
         if constexpr (M == 4) {
-            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, 0);
+            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, kStream);
         } else if constexpr (M == 5) {  // 4-byte aligned vector store + one float
-            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, 0);
-            buffer_store_f32(yy[i * M + 4], yrs, voff + 16u, so, 0);
+            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, kStream);
+            buffer_store_f32(yy[i * M + 4], yrs, voff + 16u, so, kStream);
         } else {
 #pragma unroll
             for (int jj = 0; jj < M; jj += 2)
-                buffer_store_f32x2(floatx2{yy[i * M + jj], yy[i * M + jj + 1]}, yrs, voff + 4u * jj, so, 0);
+                buffer_store_f32x2(floatx2{yy[i * M + jj], yy[i * M + jj + 1]}, yrs, voff + 4u * jj, so, kStream);
         }
     }
 }
