@@ -151,9 +151,12 @@ __device__ void buffer_store_f32(float v, int32x4 rsrc, unsigned voffset, unsign
 // Cache-policy bit of a buffer access that makes it coherent across the device
 // (the coherence that device-scope atomic loads and stores use).
 constexpr int kDeviceCoherent = 1 << 4;
-// Cache-policy bit of a streaming (non-temporal) access: the output, written once,
-// is not kept in L2 at the expense of the transformed kernels.
+// Cache-policy bit of a streaming (non-temporal) access.  An output larger than
+// the Infinity Cache, written once, is stored this way so that it does not push
+// input tiles that another output-channel group still needs, or the transformed
+// kernels, out of L2; a smaller output is better left in the caches.
 constexpr int kStream = 1 << 1;
+constexpr long long kStreamOutputBytes = 128ll << 20;
 
 __device__ __forceinline__ int32x4 make_rsrc(const float *base, unsigned bytes) {
     const unsigned long long p = reinterpret_cast<unsigned long long>(base);
@@ -656,21 +659,22 @@ __device__ __forceinline__ void store_rows(float *__restrict__ yp, const float *
 // The same through a buffer resource over y: the tile's first element at byte
 // offset voff (per lane) + soff (uniform), rows rowb bytes apart (uniform), so the
 // per-row and per-channel steps are scalar adds.
-template <int M>
+template <int M, bool STREAM>
 __device__ __forceinline__ void store_rows_buf(int32x4 yrs, unsigned voff, unsigned soff, unsigned rowb,
                                                const float *yy) {
+    constexpr int kAux = STREAM ? kStream : 0;
 #pragma unroll
     for (int i = 0; i < M; ++i) {
         const unsigned so = soff + (unsigned)i * rowb;
         if constexpr (M == 4) {
-            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, kStream);
+            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, kAux);
         } else if constexpr (M == 5) {  // 4-byte aligned vector store + one float
-            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, kStream);
-            buffer_store_f32(yy[i * M + 4], yrs, voff + 16u, so, kStream);
+            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, kAux);
+            buffer_store_f32(yy[i * M + 4], yrs, voff + 16u, so, kAux);
         } else {
 #pragma unroll
             for (int jj = 0; jj < M; jj += 2)
-                buffer_store_f32x2(floatx2{yy[i * M + jj], yy[i * M + jj + 1]}, yrs, voff + 4u * jj, so, kStream);
+                buffer_store_f32x2(floatx2{yy[i * M + jj], yy[i * M + jj + 1]}, yrs, voff + 4u * jj, so, kAux);
         }
     }
 }
@@ -961,7 +965,7 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
                                            unsigned *skc,
                                            const floatx4 *__restrict__ wt, float *__restrict__ y,
                                            const Geometry &g, const WsSeq &sq, const WsSplit &sp,
-                                           int n_inner, int kbl, int lane, int vec) {
+                                           int n_inner, int kbl, int lane, int vec, bool ystream) {
     constexpr int T = M + 2, F4 = freq_quads<M>();
     constexpr int R = 16 * TB, CC = 256 / R, SS = CC / 4, BUF = F4 * CC * R;
     constexpr int NSLOT = ws_slots<M>();
@@ -1128,7 +1132,10 @@ __device__ __forceinline__ void ws_consume(const floatx4 *lds, float *comb, unsi
             if (whole) {
                 const unsigned vb = (unsigned)((((long long)ti.n * g.K + (k_out - v)) * HW +
                                                 (long long)ti.ty * M * g.W + ti.tx * M) * 4);
-                store_rows_buf<M>(yrs, vb, (unsigned)v * hwb, rowb, yy);
+                if (ystream)
+                    store_rows_buf<M, true>(yrs, vb, (unsigned)v * hwb, rowb, yy);
+                else
+                    store_rows_buf<M, false>(yrs, vb, (unsigned)v * hwb, rowb, yy);
             } else if (ti.ok && k_out < g.K)
                 store_tile<M>(y + ((long long)ti.n * g.K + k_out) * HW, yy, ti.ty * M, ti.tx * M, g, vec != 0);
         };
@@ -1245,7 +1252,7 @@ template <int M, int TB, int FS, bool VX, bool SPLIT, bool KM>
 __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__ x,
                                                        const floatx4 *__restrict__ wt,
                                                        float *__restrict__ y, Geometry g, int vec,
-                                                       int n_inner, int n_items, WsSplit sp) {
+                                                       int n_inner, int n_items, WsSplit sp, int ystream) {
     constexpr int T = M + 2, T2 = T * T, F4 = freq_quads<M>();
     constexpr int R = 16 * TB;
     constexpr int CC = 256 / R;
@@ -1374,10 +1381,10 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
     // ---------------- consumers ----------------
     const int kbl = wave / FS;
     if constexpr (FS == 1) {
-        ws_consume<M, TB, 1, 0, SPLIT, KM>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_inner, kbl, lane, vec);
+        ws_consume<M, TB, 1, 0, SPLIT, KM>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_inner, kbl, lane, vec, ystream != 0);
     } else {
-        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0, SPLIT, KM>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_inner, kbl, lane, vec);
-        else ws_consume<M, TB, FS, 1, SPLIT, KM>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_inner, kbl, lane, vec);
+        if ((wave % FS) == 0) ws_consume<M, TB, FS, 0, SPLIT, KM>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_inner, kbl, lane, vec, ystream != 0);
+        else ws_consume<M, TB, FS, 1, SPLIT, KM>(lds, comb, pairc, ring, skc, wt, y, g, sq, sp, n_inner, kbl, lane, vec, ystream != 0);
     }
 }
 
@@ -1838,9 +1845,10 @@ static void launch_ws_t(const Geometry &g, const float *x, const float *wt, floa
     const bool km = si.n_kgroups > 1 &&
                     (double)g.T2 * g.C * g.K > (double)g.N * g.C * g.H * g.W;
     const int n_inner = km ? si.n_items / si.n_kgroups : si.n_kgroups;
+    const int ystream = (long long)g.N * g.K * g.H * g.W * 4 >= kStreamOutputBytes ? 1 : 0;
     auto go = [&](auto kern) {
         hipLaunchKernelGGL(kern, grid, block, 0, s, x, reinterpret_cast<const floatx4 *>(wt), y, g, vec ? 1 : 0,
-                           n_inner, si.n_items, sp);
+                           n_inner, si.n_items, sp, ystream);
     };
     // layers whose items all stay whole run an instantiation without the split path
     const bool split = si.n_tail > 0;
