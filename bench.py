@@ -9,20 +9,24 @@ The metric is the effective rate, direct-convolution flops (2*N*C*K*H*W*9) per
 second.  The JSON line also carries the fused kernel's own rate against the
 fp32 matrix-core roofline (transform-domain flops 2*T^2*tiles*C*K over the
 kernel's average duration, timed with HIP events on the stream it runs on), the
-three-stage variant's step time on the same layer, and the CPU oracle timed on
-the host cores.
+three-stage variant's step time on the same layer, a per-layer table of every
+configured (layer, m) pair ("layers": fused and three-stage call and kernel
+times, matrix-core and HBM fractions of the kernels), and the CPU oracle timed
+on the host cores.  The per-layer table runs before the headline's W warm-up
+steps, so the headline is measured with the shader clock at its steady level.
 
-    python bench.py [--steps K] [--warmup W] [--layer ID --m M] [--all] [--no-cpu]
+    python bench.py [--steps K] [--warmup W] [--layer ID --m M] [--all] [--no-cpu] [--no-layers]
 
 --all adds a per-(layer, m, algorithm) table (stderr, and --out): back-to-back step
 time, the median of single calls warm and cold (a 512 MB scratch write before each
 cold call evicts L2 and the Infinity Cache), and the transform-domain kernel time;
-plus, per layer, the m and algorithm a tuned plan picks (algo "tuned"), and on
-layers with C >= 128 the fused kernel with every work item split into 2 and 4
-channel pieces (algo "fused_csplitP"); and per layer the FFT-tile algorithm
-(algo "fft", 16 x 16 tiles; its "transform-domain" rate counts the real flops
-of its complex products); and for the launch-bound 56x56 layer at F(2) one call
-captured in a HIP graph and replayed (algo "fused_graph").
+plus, per layer, the m, blocking and algorithm a tuned plan picks (algo "tuned"),
+each fused blocking the library is built for at the layer's tile sizes (algo
+"fused_R<r>_K<k>"), and on layers with C >= 128 the fused kernel with every work
+item split into 2 and 4 channel pieces (algo "fused_csplitP"); and per layer the
+FFT-tile algorithm (algo "fft", 16 x 16 tiles; its "transform-domain" rate counts
+the real flops of its complex products); and for the launch-bound 56x56 layer at
+F(2) one call captured in a HIP graph and replayed (algo "fused_graph").
 """
 
 import argparse
@@ -50,6 +54,7 @@ def parse():
     ap.add_argument("--m", type=int, default=4)
     ap.add_argument("--all", action="store_true", help="also time every (layer, m, algorithm)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-layers", action="store_true", help="skip the per-layer table")
     ap.add_argument("--out", default=None, help="append the per-pair table (JSON lines) here")
     return ap.parse_args()
 
@@ -129,8 +134,10 @@ def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False, tuning=None):
         wt_ms = sum(a.elapsed_time(b) for a, b, _ in evs) / steps
         body_ms = sum(b.elapsed_time(c) for _, b, c in evs) / steps
         nt, dflops, tflops = p.info()
+        p.status()
         res = {"ms_per_step": ms_step, "weight_transform_ms": wt_ms, "body_ms": body_ms,
-               "direct_flops": dflops, "tdomain_flops": tflops, "tiles": nt}
+               "direct_flops": dflops, "tdomain_flops": tflops, "tiles": nt,
+               "kernel": p.describe(), "params": p.params()}
         if per_call:
             res["warm_call_ms_median"] = rep_times(p, x, w, y, steps, stream)
             scratch = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
@@ -180,6 +187,66 @@ def time_graph(layer, m, steps, warmup, x, w):
     return ms_step, sorted(single)[len(single) // 2]
 
 
+def algorithmic_bytes(layer, m, algo, kit=64):
+    """Minimal HBM bytes of the transform-domain part of one call: the fused kernel
+    reads x and the transformed kernels W' and writes y; the three-stage pipeline
+    also writes and reads U (T^2 x tiles x C) and M (T^2 x tiles x K)."""
+    T2 = (m + 2) ** 2
+    tiles = layer.N * -(-layer.H // m) * -(-layer.W // m)
+    x = 4 * layer.N * layer.C * layer.H * layer.W
+    y = 4 * layer.N * layer.K * layer.H * layer.W
+    wt = 4 * T2 * layer.C * layer.K
+    if algo == "fused":
+        return x + y + wt
+    return x + 2 * 4 * T2 * tiles * layer.C + wt + 2 * 4 * T2 * tiles * layer.K + y
+
+
+def layer_table(steps=20, warmup=10):
+    """Every configured (layer, m) pair, fused and three-stage: call time, kernel
+    (transform-domain) time, and the kernels' fractions of the fp32 matrix peak
+    and of the HBM peak (algorithmic bytes over kernel time)."""
+    import torch
+    from paper_1912_02165_amd import workloads
+    rows = []
+    for lay in workloads.LAYERS:
+        xn, wn = workloads.layer_inputs(lay)
+        xa, wa = torch.from_numpy(xn).cuda(), torch.from_numpy(wn).cuda()
+        del xn, wn
+        for m in lay.ms:
+            row = {"workload": lay.tag(m)}
+            for algo in ("fused", "three_stage"):
+                r = time_pair(lay, m, algo, steps, warmup, xa, wa)
+                ms = r["body_ms"] * 1e-3
+                row[algo] = {
+                    "ms_per_call": r["ms_per_step"],
+                    "kernel_ms": r["body_ms"],
+                    "eff_tflops": r["direct_flops"] / (r["ms_per_step"] * 1e-3) / 1e12,
+                    "mfma_frac": r["tdomain_flops"] / ms / P_MFMA_F32,
+                    "hbm_frac": algorithmic_bytes(lay, m, algo) / ms / B_HBM,
+                    "kernel": r["kernel"],
+                }
+            row["fused_speedup_over_three_stage"] = (row["three_stage"]["kernel_ms"]
+                                                     / row["fused"]["kernel_ms"])
+            rows.append(row)
+            print(json.dumps(row), file=sys.stderr, flush=True)
+        del xa, wa
+    return rows
+
+
+def host_cpu():
+    """(nproc, CPU model name) of the host."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return os.cpu_count(), model
+
+
 def cpu_baseline(layer, budget_s=20.0):
     """The oracle (plain C direct convolution, fp64 accumulation, OpenMP) on the first
     images of the layer: one image to size the sample, then as many images as fit in
@@ -199,8 +266,9 @@ def cpu_baseline(layer, budget_s=20.0):
     else:
         dt = t1
     flops = layer.direct_flops / layer.N * n
+    nproc, model = host_cpu()
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": direct.num_threads(),
-            "kind": "oracle",
+            "nproc": nproc, "cpu_model": model, "kind": "oracle",
             "sample": f"{n} of {layer.N} images of {layer.name} (direct conv, fp64 accumulation), "
                       f"{dt:.2f} s"}
 
@@ -215,6 +283,7 @@ def main():
     import torch
     from paper_1912_02165_amd import workloads
 
+    layers = None if args.no_layers else layer_table()
     layer = workloads.LAYER_BY_ID[args.layer]
     m = args.m
     x_np, w_np = workloads.layer_inputs(layer)
@@ -245,13 +314,16 @@ def main():
                    "W": layer.W, "m": m, "algo": "fused", "stride": 1, "pad": 1},
         "roofline": {"bound": "mfma", "achieved": achieved / 1e12, "peak": P_MFMA_F32 / 1e12,
                      "unit": "TFLOP/s", "frac": achieved / P_MFMA_F32, "traffic": traffic,
-                     "kernel": "fused_kernel", "kernel_ms": kernel_ms},
+                     "kernel": fused["kernel"], "kernel_ms": kernel_ms,
+                     "kernel_ms_timing": "HIP events around run_pretransformed on its stream, "
+                                         "mean of the timed steps"},
         "tdomain_tflops_per_step": fused["tdomain_flops"] / (fused["ms_per_step"] * 1e-3) / 1e12,
         "weight_transform_ms": fused["weight_transform_ms"],
         "three_stage": {"ms_per_step": three["ms_per_step"],
                         "value": three["direct_flops"] / (three["ms_per_step"] * 1e-3) / 1e12,
                         "body_ms": three["body_ms"]},
         "cpu_baseline": None,
+        "layers": layers,
     }
     if not args.no_cpu:
         rec["cpu_baseline"] = cpu_baseline(layer)
@@ -265,11 +337,17 @@ def main():
             xn, wn = workloads.layer_inputs(lay)
             xa, wa = torch.from_numpy(xn).cuda(), torch.from_numpy(wn).cuda()
             cases = [(mm, "fused", "fused"), (mm, "three_stage", "three_stage")]
+            # every built fused blocking at this tile size
+            cases += [(mm, "fused", "fused_R%d_K%d" % (R, kit))
+                      for (bm, R, kit) in wc.wino_fused_blockings() if bm == mm]
+            tuned_blocking = None
             if lay.id not in tuned_done:
-                # the tile size and algorithm a per-layer tuning picks (timed now)
+                # the tile size, blocking and algorithm a per-layer tuning picks (timed now)
                 tuned_done.add(lay.id)
                 tp = wc.Plan.tuned(lay.N, lay.C, lay.K, lay.H, lay.W,
                                    wc.WINO_TUNE_ALL_M | wc.WINO_TUNE_THREE_STAGE)
+                _, _, tR, tkit = tp.params()
+                tuned_blocking = (tR, tkit)
                 cases.append((tp.m, tp.algo, "tuned"))
                 tp.close()
             if lay.C >= 128:
@@ -283,6 +361,11 @@ def main():
                 tuning = None
                 if label.startswith("fused_csplit"):
                     tuning = {"channel_splits": int(label[len("fused_csplit"):])}
+                elif label.startswith("fused_R"):
+                    R, kit = (int(v) for v in label[len("fused_R"):].split("_K"))
+                    tuning = {"tiles_per_wg": R, "k_per_wg": kit}
+                elif label == "tuned" and algo == "fused":
+                    tuning = {"tiles_per_wg": tuned_blocking[0], "k_per_wg": tuned_blocking[1]}
                 r = time_pair(lay, m_c, algo, args.steps, args.warmup, xa, wa, per_call=True,
                               tuning=tuning)
                 wl = lay.name + "/FFT(16x16 tiles)" if algo == "fft" else lay.tag(m_c)
@@ -295,8 +378,11 @@ def main():
                        "tdomain_tflops_body": r["tdomain_flops"] / (r["body_ms"] * 1e-3) / 1e12,
                        "mfma_frac_body": r["tdomain_flops"] / (r["body_ms"] * 1e-3) / P_MFMA_F32,
                        "weight_transform_ms": r["weight_transform_ms"]}
+                row["kernel"] = r["kernel"]
                 if label == "tuned":
-                    row["tuned_choice"] = {"m": m_c, "algo": algo}
+                    row["tuned_choice"] = {"m": m_c, "algo": algo,
+                                           "tiles_per_wg": tuned_blocking[0] if algo == "fused" else 0,
+                                           "k_per_wg": tuned_blocking[1] if algo == "fused" else 0}
                 rows.append(row)
                 print(json.dumps(row), file=sys.stderr, flush=True)
             if lay.id == 1 and mm == 2:

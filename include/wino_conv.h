@@ -58,7 +58,8 @@ enum {
     WINO_EINVAL = -1,       /* bad argument */
     WINO_EUNSUPPORTED = -2, /* valid request this library does not handle */
     WINO_ENOMEM = -3,       /* device allocation failed */
-    WINO_EHIP = -4          /* a HIP call or kernel launch failed */
+    WINO_EHIP = -4,         /* a HIP call or kernel launch failed */
+    WINO_EKERNEL = -5       /* a kernel reported a failure through the plan's status word */
 };
 
 enum {
@@ -74,47 +75,40 @@ enum {
     WINO_BUF_PRODUCT = 2    /* three-stage only: per-frequency products    */
 };
 
-/* Fused-kernel schedules (wino_tuning.schedule). */
-enum {
-    WINO_SCHED_AUTO = 0,
-    WINO_SCHED_SHARED = 1,      /* a workgroup transforms each input tile once into LDS and
-                                   shares it across 64 output channels */
-    WINO_SCHED_PER_WAVE = 2,    /* every wave transforms its own input tiles in registers */
-    WINO_SCHED_SPECIALISED = 3, /* default: persistent workgroups (one per compute unit) whose
-                                   producer waves load and transform input tiles into an LDS
-                                   stage ring while consumer waves run the products and the
-                                   output transform; the last round of work items is split
-                                   across workgroups when few rounds would leave units idle */
-    WINO_SCHED_PERSISTENT = 4   /* F(2x2,3x3) only: persistent, one wave per SIMD doing both */
-};
-
-/* Optional blocking overrides for the fused algorithm; a field of 0 keeps the
- * automatic choice.
- *   schedule:          WINO_SCHED_*.
- *   k_blocks_per_wave: per-wave schedule: output channels per wave, in blocks of 16.
- *   waves_per_group:   per-wave schedule: waves (16 tiles each) per workgroup, 1..4.
- *   tile_blocks:       shared schedule: tiles per workgroup in blocks of 16 (1, or 2
- *                      for m <= 4).
- *   channel_splits:    specialised schedule (fused algorithm only): compute the
- *                      layer as P convolutions over disjoint, consecutive subsets
- *                      of the input channels and add their outputs (Sec. 7 on
- *                      splitting channels; the output transform is linear, so each
- *                      subset's products are inverse-transformed on their own).
- *                      Every work item (16 tiles x 64 output channels; 32 tiles
- *                      for m = 2, 32 channels for m >= 5) is cut into pieces of L = ceil(S / channel_splits)
- *                      channel stages, S = ceil(C / 16) (ceil(C / 8) for m = 2),
- *                      so P = ceil(S / L) pieces, at most S.  The pieces' outputs
- *                      go to a plan-owned buffer of P partial tiles per item and
- *                      are added in channel order by the piece that finishes last
- *                      (results do not depend on the order pieces run in, but
- *                      differ from the unsplit sum by rounding).  0 or 1: no
- *                      split; at most WINO_MAX_CHANNEL_SPLITS. */
+/* Optional blocking of the fused algorithm (the task of Sec. 4.1: a workgroup
+ * transforms R input tiles, multiplies them by the transformed kernels of a
+ * group of output channels over all input channels, and inverse-transforms the
+ * results, all on chip).  A field of 0 keeps the automatic choice.
+ *   tiles_per_wg:   R, tiles per task: 16, or 32 for m = 2.
+ *   k_per_wg:       output channels per task: 64, 32 or 16.  Built (m, R, k):
+ *                   m = 2: (32, 64), (16, 64), (32, 32), (16, 32), (16, 16);
+ *                   m = 4: (16, 64), (16, 32);  m = 5, 6: (16, 32), (16, 16).
+ *                   The task's result matrices (R x k x T^2 floats) live in
+ *                   registers, which bounds R * k (Sec. 4.1's private capacity).
+ *   c_chunk:        input channels per pipeline stage; it is 256 / R (each of the
+ *                   256 producer lanes transforms one (tile, channel) pair per
+ *                   stage), so only 0 or that value is accepted.
+ *   channel_splits: compute the layer as P convolutions over disjoint,
+ *                   consecutive subsets of the input channels and add their
+ *                   outputs (Sec. 7 on splitting channels; the output transform
+ *                   is linear, so each subset's products are inverse-transformed
+ *                   on their own).  Every work item is cut into pieces of
+ *                   L = ceil(S / channel_splits) channel stages, S = ceil(C /
+ *                   c_chunk), so P = ceil(S / L) pieces, at most S.  The pieces'
+ *                   outputs go to a plan-owned buffer of P partial tiles per item
+ *                   and are added in channel order by the piece that finishes last
+ *                   (results do not depend on the order pieces run in, but differ
+ *                   from the unsplit sum by rounding).  0 or 1: no split; at most
+ *                   WINO_MAX_CHANNEL_SPLITS.
+ * Automatic choice (wino_conv_plan): the largest R and k that fit (most reuse of
+ * each transformed input tile and transformed-kernel operand), unless a
+ * smaller k fills the compute units with enough more work items to be
+ * estimated at least 10 % faster; wino_conv_plan_tuned measures instead. */
 #define WINO_MAX_CHANNEL_SPLITS 64
 typedef struct {
-    int schedule;
-    int k_blocks_per_wave;
-    int waves_per_group;
-    int tile_blocks;
+    int tiles_per_wg;
+    int k_per_wg;
+    int c_chunk;
     int channel_splits;
 } wino_tuning;
 
@@ -193,6 +187,31 @@ int wino_conv_intermediate_dims(const wino_plan *p, int which, long long dims[4]
  * null stream after a device synchronisation).  Returns WINO_EINVAL if the plan
  * has no such buffer or count is larger than it. */
 int wino_conv_copy_intermediate(const wino_plan *p, int which, float *host_dst, size_t count);
+
+/* Synchronous check of the plan's status word.  The persistent fused kernel's
+ * producer and consumer waves hand stages to each other through counters in
+ * shared memory; every wait is bounded (it gives up after about 4 million polls
+ * rather than hang the GPU), and a wait that gives up sets a bit in a device word
+ * the plan owns.  A call whose wait gave up has queued without error but its y is
+ * not valid.  This function waits for all work on the device
+ * (hipDeviceSynchronize), reads the word, and if it is nonzero clears it and the
+ * plan's split arrival counters and returns WINO_EKERNEL (wino_last_error names
+ * the bits); otherwise WINO_OK.  WINO_EINVAL for a NULL plan, WINO_EHIP if a HIP
+ * call fails. */
+int wino_conv_status(const wino_plan *p);
+
+/* Test hook for the status plumbing: writes `word` into the plan's status word
+ * (synchronous copy), as a kernel whose wait gave up would.  Returns WINO_OK,
+ * WINO_EINVAL for a NULL plan, WINO_EHIP if the copy fails. */
+int wino_conv_debug_set_status(const wino_plan *p, unsigned word);
+
+/* One line of text naming the kernel(s) a call of the plan launches and their
+ * blocking: for the fused algorithm the kernel and its template parameters, the
+ * tiles per task R and output channels per task, channels per stage, work items,
+ * grid and split pieces; for the three-stage algorithm its three kernels.  The
+ * text (NUL-terminated, truncated to len - 1 characters) goes to buf.  Returns
+ * WINO_EINVAL for a NULL plan or buffer or len == 0. */
+int wino_conv_describe(const wino_plan *p, char *buf, size_t len);
 
 /* Message describing the last failure on the calling thread ("" if none). */
 const char *wino_last_error(void);

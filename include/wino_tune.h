@@ -3,20 +3,23 @@
  *
  * Sec. 6 runs one fixed configuration on every layer and notes that tuning the
  * parameters for each particular layer can only improve the results; Sec. 7
- * says that tuning is done once and stored in a wisdom file.  Here the tuned
- * parameter is the tile size m of F(m x m, 3 x 3), m in {2, 4, 5, 6} (the
- * paper's T = m + 2; the number of tiles per task is fixed by the matrix-core
- * blocking) and, optionally, the algorithm (fused or three-stage at each m, or
- * the FFT-tile algorithm with m = 14).  A tuning result is remembered per
- * (GPU architecture, compute units, N, C, K, H, W, candidate set) in a
- * process-wide wisdom table that can be written to and read from a text file.
+ * says that the parameters (R, the tiles per task, among them) can be tuned once
+ * and stored in a wisdom file.  Here the tuned parameters are the tile size m of
+ * F(m x m, 3 x 3), m in {2, 4, 5, 6} (the paper's T = m + 2), the fused kernel's
+ * blocking at each m -- tiles per task R and output channels per task, every
+ * blocking the kernel is built for (wino_fused_blockings) -- and, optionally,
+ * the algorithm (three-stage at each m, or the FFT-tile algorithm with m = 14).
+ * A tuning result is remembered per (GPU architecture, compute units, N, C, K,
+ * H, W, candidate set) in a process-wide wisdom table that can be written to and
+ * read from a text file.
  *
  * Wisdom file: text, one entry per line, '#' starts a comment line:
- *     <arch> <cus> <N> <C> <K> <H> <W> <candidates> <m> <algo> <microseconds>
+ *     <arch> <cus> <N> <C> <K> <H> <W> <candidates> <m> <algo> <R> <k> <microseconds>
  * arch is the device's architecture name (e.g. gfx950), candidates is the
  * candidate mask in hexadecimal (0x...), algo is 0 (fused), 1 (three-stage) or
- * 2 (FFT, with m = 14)
- * and microseconds the measured time of one call.
+ * 2 (FFT, with m = 14), R and k the fused blocking (tiles and output channels per
+ * task; 0 0 for the other algorithms) and microseconds the measured time of one
+ * call.
  *
  * Thread safety: the wisdom table is guarded by a lock; plans are as in
  * wino_conv.h (one stream at a time).
@@ -42,8 +45,8 @@ enum {
 };
 
 /* A plan for the convolution of wino_conv_plan (N x C x H x W input, K output
- * channels) with the m and algorithm that run fastest on the current device
- * among the candidates (a nonzero mask of WINO_TUNE_* bits with at least one
+ * channels) with the m, fused blocking and algorithm that run fastest on the
+ * current device among the candidates (a nonzero mask of WINO_TUNE_* bits with at least one
  * WINO_TUNE_M* or the WINO_TUNE_FFT bit).  If the wisdom table holds the answer it is used directly;
  * otherwise every candidate is planned and timed here: its kernels transformed
  * once, then the median of 5 calls of wino_conv_run_pretransformed after 10
@@ -57,14 +60,22 @@ enum {
 wino_plan *wino_conv_plan_tuned(int N, int C, int K, int H, int W, unsigned candidates,
                                 int *chosen_m, int *chosen_algo, double *call_us);
 
-/* The tile size m and algorithm of a plan.  Returns WINO_EINVAL for NULL. */
-int wino_conv_plan_params(const wino_plan *p, int *m, int *algo);
+/* The tile size m, algorithm and fused blocking (tiles and output channels per
+ * task; 0 for the other algorithms) of a plan.  Any output pointer may be NULL.
+ * Returns WINO_EINVAL for a NULL plan. */
+int wino_conv_plan_params(const wino_plan *p, int *m, int *algo, int *tiles_per_wg, int *k_per_wg);
 
-/* Look up an entry: on WINO_OK, *found is 1 and *m, *algo hold the entry, or
- * *found is 0.  arch is an architecture name as in the file.  Returns
- * WINO_EINVAL for NULL pointers. */
+/* The fused blockings the library is built for: up to max (m, tiles_per_wg,
+ * k_per_wg) triples are written to the arrays (each may be NULL); returns the
+ * total number. */
+int wino_fused_blockings(int *m, int *tiles_per_wg, int *k_per_wg, int max);
+
+/* Look up an entry: on WINO_OK, *found is 1 and *m, *algo, *tiles_per_wg,
+ * *k_per_wg hold the entry, or *found is 0.  arch is an architecture name as in
+ * the file.  Returns WINO_EINVAL for NULL pointers. */
 int wino_wisdom_lookup(const char *arch, int cus, int N, int C, int K, int H, int W,
-                       unsigned candidates, int *found, int *m, int *algo);
+                       unsigned candidates, int *found, int *m, int *algo, int *tiles_per_wg,
+                       int *k_per_wg);
 
 /* Write the table to path (replacing the file).  Returns WINO_EINVAL if the
  * file cannot be written. */

@@ -26,17 +26,23 @@
 #include <hip/hip_runtime.h>
 
 namespace wino {
-namespace {
 
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef int int32x4 __attribute__((ext_vector_type(4)));
+typedef float fft_floatx4 __attribute__((ext_vector_type(4)));
+typedef int fft_int32x4 __attribute__((ext_vector_type(4)));
 
 // Raw buffer loads: an offset at or past the resource's size reads 0, which
-// gives the zero padding of input windows without branches.
-__device__ float fft_buffer_load_f32(int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+// gives the zero padding of input windows without branches.  (Declared outside
+// the anonymous namespace below: they name LLVM intrinsics, which have external
+// linkage.)
+__device__ float fft_buffer_load_f32(fft_int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
     __asm("llvm.amdgcn.raw.buffer.load.f32");
-__device__ void fft_buffer_store_f32(float v, int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
+__device__ void fft_buffer_store_f32(float v, fft_int32x4 rsrc, unsigned voffset, unsigned soffset, int aux)
     __asm("llvm.amdgcn.raw.buffer.store.f32");
+
+namespace {
+
+typedef fft_floatx4 floatx4;
+typedef fft_int32x4 int32x4;
 __device__ __forceinline__ int32x4 fft_rsrc(const float *base, unsigned bytes) {
     const unsigned long long p = reinterpret_cast<unsigned long long>(base);
     int32x4 r;

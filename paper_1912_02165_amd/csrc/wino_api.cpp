@@ -219,35 +219,41 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         return nullptr;
     }
     if (make_geometry(N, C, K, H, W, m, algo, &g) != WINO_OK) return nullptr;
-    FusedCfg cfg = wino::fused_cfg_default(g);
+    // blocking overrides (checked here, before any HIP call)
+    int want_R = 0, want_kit = 0, csplit = 0;
     if (t) {
-        if (t->schedule < 0 || t->k_blocks_per_wave < 0 || t->waves_per_group < 0 ||
-            t->tile_blocks < 0 || t->channel_splits < 0) {
+        if (t->tiles_per_wg < 0 || t->k_per_wg < 0 || t->c_chunk < 0 || t->channel_splits < 0) {
             set_err("tuning fields must be >= 0");
             return nullptr;
         }
-        if (t->schedule) cfg.schedule = t->schedule;
-        if (t->k_blocks_per_wave) cfg.nkb = t->k_blocks_per_wave;
-        if (t->waves_per_group) cfg.waves = t->waves_per_group;
-        if (t->tile_blocks) cfg.tb = t->tile_blocks;
-        if (t->channel_splits > 1) {
-            if (algo != WINO_ALGO_FUSED || cfg.schedule != wino::kSchedSpecialised) {
-                set_err("channel_splits=%d needs the fused algorithm with the specialised schedule",
-                        t->channel_splits);
+        if ((t->tiles_per_wg || t->k_per_wg || t->c_chunk || t->channel_splits > 1) && algo != WINO_ALGO_FUSED) {
+            set_err("blocking overrides apply to the fused algorithm only");
+            return nullptr;
+        }
+        want_R = t->tiles_per_wg;
+        want_kit = t->k_per_wg;
+        if (t->c_chunk) {
+            const int R = want_R ? want_R : (m == 2 ? 32 : 16);
+            if (t->c_chunk * R != 256) {
+                set_err("c_chunk=%d: a stage holds 256 / tiles_per_wg = %d input channels", t->c_chunk, 256 / R);
                 return nullptr;
             }
+            want_R = R;
+        }
+        bool any = false;
+        for (const wino::FusedBlocking &b : wino::kFusedBlockings)
+            if (b.m == m && (!want_R || b.R == want_R) && (!want_kit || b.kit == want_kit)) any = true;
+        if (algo == WINO_ALGO_FUSED && !any) {
+            set_err("fused blocking tiles_per_wg=%d k_per_wg=%d is not built for m=%d", want_R, want_kit, m);
+            return nullptr;
+        }
+        if (t->channel_splits > 1) {
             if (t->channel_splits > WINO_MAX_CHANNEL_SPLITS) {
                 set_err("channel_splits=%d exceeds %d", t->channel_splits, WINO_MAX_CHANNEL_SPLITS);
                 return nullptr;
             }
-            cfg.csplit = t->channel_splits;
+            csplit = t->channel_splits;
         }
-    }
-    if (algo == WINO_ALGO_FUSED && !wino::fused_cfg_supported(m, cfg)) {
-        set_err("fused schedule %d (k_blocks_per_wave=%d waves_per_group=%d tile_blocks=%d) "
-                "is not built for m=%d",
-                cfg.schedule, cfg.nkb, cfg.waves, cfg.tb, m);
-        return nullptr;
     }
     // frequencies in float4 groups, the last one padded when T^2 is odd (F(5));
     // FFT: a float4 {Re, Im, -Im, 0} per frequency
@@ -258,6 +264,13 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
     if (algo == WINO_ALGO_THREE_STAGE) {
         U_bytes = (size_t)g.T2 * g.Cs * 4 * g.tiles_p * sizeof(float);
         M_bytes = (size_t)g.T2 * g.Kb_alloc * 16 * g.tiles_p * sizeof(float);
+    }
+    // The kernels address the transformed kernels, the input and the output with
+    // 32-bit byte offsets (buffer resources): each must stay below 2^32 bytes.
+    if (wt_bytes >= (size_t(1) << 32)) {
+        set_err("problem too large: the transformed kernels take %zu bytes, the kernels address "
+                "at most 2^32 (C=%d K=%d m=%d)", wt_bytes, C, K, m);
+        return nullptr;
     }
     if (fail_alloc_forced()) {
         set_err("device allocation of %zu bytes failed (forced by WINO_TEST_FAIL_ALLOC)",
@@ -271,6 +284,7 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         hip_fail("hipGetDevice", e);
         return nullptr;
     }
+    int num_cus = 256;
     {
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -278,7 +292,12 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
             (void)hipGetLastError();
             cus = 256;
         }
-        cfg.num_cus = cus;
+        num_cus = cus;
+    }
+    FusedCfg cfg{0, 0, num_cus, csplit};
+    if (algo == WINO_ALGO_FUSED) {
+        cfg = wino::fused_cfg_default(g, num_cus, want_R, want_kit);
+        cfg.csplit = csplit;
     }
     size_t part_bytes = 0, cnt_bytes = 0;
     if (algo == WINO_ALGO_FUSED) {
@@ -288,7 +307,9 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
             cnt_bytes = (size_t)si.n_tail * sizeof(unsigned);
         }
     }
-    const size_t total_bytes = wt_bytes + U_bytes + M_bytes + part_bytes + cnt_bytes;
+    // status word (wino_conv_status), 256 bytes so the allocation is its own cache line
+    const size_t err_bytes = 256;
+    const size_t total_bytes = wt_bytes + U_bytes + M_bytes + part_bytes + cnt_bytes + err_bytes;
     wino_plan *p = new (std::nothrow) wino_plan();
     if (!p) {
         set_err("host allocation failed");
@@ -312,6 +333,9 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         if ((e = hipMalloc(&ptr, M_bytes)) != hipSuccess) goto oom;
         p->Mf = static_cast<float *>(ptr);
     }
+    if ((e = hipMalloc(&ptr, err_bytes)) != hipSuccess) goto oom;
+    p->split.err = static_cast<unsigned *>(ptr);
+    if ((e = hipMemset(p->split.err, 0, err_bytes)) != hipSuccess) goto oom;
     if (part_bytes) {
         if ((e = hipMalloc(&ptr, part_bytes)) != hipSuccess) goto oom;
         p->split.part = static_cast<float *>(ptr);
@@ -320,15 +344,15 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
         // arrival counters start at zero; each split item's last contributor
         // resets its counter, so they are zero again after every call
         if ((e = hipMemset(p->split.cnt, 0, cnt_bytes)) != hipSuccess) goto oom;
-        if ((e = hipDeviceSynchronize()) != hipSuccess) goto oom;
     }
+    if ((e = hipDeviceSynchronize()) != hipSuccess) goto oom;
     if (log_enabled())
         fprintf(stderr,
-                "[wino] plan N=%d C=%d K=%d H=%d W=%d m=%d algo=%s tiles=%d schedule=%d tb=%d "
-                "nkb=%d waves=%d channel_splits=%d workspace=%zu B\n",
+                "[wino] plan N=%d C=%d K=%d H=%d W=%d m=%d algo=%s tiles=%d R=%d k_per_wg=%d "
+                "channel_splits=%d workspace=%zu B\n",
                 N, C, K, H, W, m,
                 algo == WINO_ALGO_FUSED ? "fused" : algo == WINO_ALGO_FFT ? "fft" : "three_stage", g.ntiles,
-                cfg.schedule, cfg.tb, cfg.nkb, cfg.waves, cfg.csplit, total_bytes);
+                cfg.R, cfg.kit, cfg.csplit, total_bytes);
     return p;
 oom:
     (void)hipGetLastError();
@@ -338,14 +362,29 @@ oom:
     return nullptr;
 }
 
-int wino_conv_plan_params(const wino_plan *p, int *m, int *algo) {
+int wino_conv_plan_params(const wino_plan *p, int *m, int *algo, int *tiles_per_wg, int *k_per_wg) {
     if (!p) {
         set_err("plan is NULL");
         return WINO_EINVAL;
     }
     if (m) *m = p->g.m;
     if (algo) *algo = p->algo;
+    if (tiles_per_wg) *tiles_per_wg = p->algo == WINO_ALGO_FUSED ? p->fcfg.R : 0;
+    if (k_per_wg) *k_per_wg = p->algo == WINO_ALGO_FUSED ? p->fcfg.kit : 0;
     return WINO_OK;
+}
+
+int wino_fused_blockings(int *m, int *tiles_per_wg, int *k_per_wg, int max) {
+    int n = 0;
+    for (const wino::FusedBlocking &b : wino::kFusedBlockings) {
+        if (n < max) {
+            if (m) m[n] = b.m;
+            if (tiles_per_wg) tiles_per_wg[n] = b.R;
+            if (k_per_wg) k_per_wg[n] = b.kit;
+        }
+        ++n;
+    }
+    return n;
 }
 
 wino_plan *wino_conv_plan(int N, int C, int K, int H, int W, int m) {
@@ -359,11 +398,60 @@ void wino_conv_destroy(wino_plan *p) {
     if (p->Mf) (void)hipFree(p->Mf);
     if (p->split.part) (void)hipFree(p->split.part);
     if (p->split.cnt) (void)hipFree(p->split.cnt);
+    if (p->split.err) (void)hipFree(p->split.err);
     delete p;
 }
 
 size_t wino_conv_workspace_bytes(const wino_plan *p) {
-    return p ? p->wt_bytes + p->U_bytes + p->M_bytes + p->part_bytes + p->cnt_bytes : 0;
+    return p ? p->wt_bytes + p->U_bytes + p->M_bytes + p->part_bytes + p->cnt_bytes + 256 : 0;
+}
+
+int wino_conv_status(const wino_plan *p) {
+    if (!p) {
+        set_err("plan is NULL");
+        return WINO_EINVAL;
+    }
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail("hipDeviceSynchronize", e);
+    unsigned word = 0;
+    e = hipMemcpy(&word, p->split.err, sizeof word, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail("hipMemcpy of the status word", e);
+    if (word == 0) return WINO_OK;
+    // clear the word, and the split arrival counters a wait that gave up may have
+    // left nonzero, so that the next call starts clean
+    e = hipMemset(p->split.err, 0, sizeof word);
+    if (e == hipSuccess && p->split.cnt) e = hipMemset(p->split.cnt, 0, p->cnt_bytes);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail("resetting the status word", e);
+    set_err("a kernel wait gave up (status 0x%x): the outputs of the calls since the last "
+            "status check are not valid", word);
+    return WINO_EKERNEL;
+}
+
+int wino_conv_describe(const wino_plan *p, char *buf, size_t len) {
+    if (!p || !buf || len == 0) {
+        set_err("plan or buffer is NULL, or len is 0");
+        return WINO_EINVAL;
+    }
+    if (p->algo == WINO_ALGO_FUSED) {
+        wino::describe_fused(p->g, p->fcfg, buf, len);
+    } else if (p->algo == WINO_ALGO_FFT) {
+        snprintf(buf, len, "fft_weight_transform_kernel, fft_fused_kernel: 16 x 16 tiles, 16 tiles x 16 output "
+                 "channels per work item");
+    } else {
+        wino::describe_three_stage(p->g, buf, len);
+    }
+    return WINO_OK;
+}
+
+int wino_conv_debug_set_status(const wino_plan *p, unsigned word) {
+    if (!p) {
+        set_err("plan is NULL");
+        return WINO_EINVAL;
+    }
+    hipError_t e = hipMemcpy(p->split.err, &word, sizeof word, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail("hipMemcpy of the status word", e);
+    return WINO_OK;
 }
 
 int wino_conv_info(const wino_plan *p, long long *n_tiles, double *direct_flops,

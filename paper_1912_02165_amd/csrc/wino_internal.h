@@ -20,16 +20,33 @@ struct Geometry {
     int tiles_p;        // ntiles rounded up to a multiple of 64 (three-stage buffers)
 };
 
-// Fused-kernel schedule and blocking.
-enum { kSchedShared = 1, kSchedPerWave = 2, kSchedSpecialised = 3, kSchedPersistent = 4 };
+// Blocking of the fused kernel (the paper's task, Sec. 4.1): R tiles and kit
+// output channels per work item; the input channels of a stage are 256 / R (one
+// (tile, channel) pair per producer lane).
 struct FusedCfg {
-    int schedule;  // kSchedShared, kSchedPerWave, kSchedSpecialised or kSchedPersistent
-    int tb;        // shared: tile blocks of 16 per workgroup
-    int nkb;       // per-wave: 16-channel output blocks per wave
-    int waves;     // per-wave: waves per workgroup (each owns 16 tiles)
+    int R;         // tiles per item: 16 or 32
+    int kit;       // output channels per item: 16, 32 or 64
     int num_cus;   // compute units of the device (persistent grid size)
-    int csplit;    // specialised: channel pieces per work item (0 or 1: whole items)
+    int csplit;    // channel pieces per work item (0 or 1: whole items)
 };
+
+// The (m, R, kit) blockings the fused kernel is built for, with the kernel
+// template of each: X(m, R, kit, TB, FS, CSP), R = 16 TB tiles, FS * CSP consumer
+// waves per 16-channel output block (wino_ws.h).  The build compiles
+// wino_fused_inst.hip once per entry.
+#define WINO_FUSED_BLOCKINGS(X)                                                                \
+    X(2, 32, 64, 2, 1, 1) X(2, 16, 64, 1, 1, 1) X(2, 32, 32, 2, 2, 1) X(2, 16, 32, 1, 1, 2)     \
+    X(2, 16, 16, 1, 2, 2) X(4, 16, 64, 1, 1, 1) X(4, 16, 32, 1, 1, 2) X(5, 16, 32, 1, 2, 1)     \
+    X(5, 16, 16, 1, 2, 2) X(6, 16, 32, 1, 2, 1) X(6, 16, 16, 1, 2, 2)
+
+struct FusedBlocking {
+    int m, R, kit;
+    int tb, fs, csp;
+};
+#define WINO_FB_ENTRY(m, R, kit, tb, fs, csp) {m, R, kit, tb, fs, csp},
+constexpr FusedBlocking kFusedBlockings[] = {WINO_FUSED_BLOCKINGS(WINO_FB_ENTRY)};
+#undef WINO_FB_ENTRY
+bool fused_blocking_built(int m, int R, int kit);
 
 // Split plan of the warp-specialised fused kernel: the last round of items (or,
 // with channel splitting, every item) is divided stage-wise among workgroups;
@@ -48,8 +65,12 @@ struct SplitInfo {
 struct SplitBuffers {
     float *part;           // n_tail * maxc * part_floats floats
     unsigned *cnt;         // n_tail arrival counters, zero between calls
+    unsigned *err;         // status word: bits set by kernel waits that gave up
 };
 SplitInfo fused_split_info(const Geometry &g, const FusedCfg &cfg);
+
+// One line naming the fused kernel a call launches and its blocking.
+void describe_fused(const Geometry &g, const FusedCfg &cfg, char *buf, size_t len);
 
 // Kernel transform: w (K x C x 3 x 3) -> wt in matrix-core operand order.
 hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt, hipStream_t s);
@@ -71,8 +92,11 @@ hipError_t launch_fft_fused(const Geometry &g, const float *x, const float *wt, 
 // Sets the message wino_last_error() returns on the calling thread (printf format).
 void set_error(const char *fmt, ...);
 
-// Fused blocking the kernels are instantiated for, per m.
-bool fused_cfg_supported(int m, const FusedCfg &cfg);
-FusedCfg fused_cfg_default(const Geometry &g);
+// Default blocking of a layer among the built ones (restricted to tiles per item
+// want_R and output channels per item want_kit where those are nonzero).
+FusedCfg fused_cfg_default(const Geometry &g, int num_cus, int want_R = 0, int want_kit = 0);
+
+// One line naming the three-stage kernels.
+void describe_three_stage(const Geometry &g, char *buf, size_t len);
 
 }  // namespace wino

@@ -1,5 +1,6 @@
-// Per-layer tuning of the tile size (and optionally the algorithm) and the wisdom
-// table that remembers the results (declared in include/wino_tune.h).
+// Per-layer tuning of the tile size, the fused kernel's blocking (tiles and output
+// channels per task) and optionally the algorithm, and the wisdom table that
+// remembers the results (declared in include/wino_tune.h).
 #include "wino_tune.h"
 #include "wino_internal.h"
 
@@ -19,6 +20,7 @@ namespace {
 using Key = std::tuple<std::string, int, int, int, int, int, int, unsigned>;  // arch, cus, N, C, K, H, W, mask
 struct Choice {
     int m, algo;
+    int R, kit;  // fused blocking (0 for the other algorithms)
     double us;
 };
 
@@ -30,12 +32,20 @@ constexpr unsigned kAllBits = kMBits | WINO_TUNE_THREE_STAGE | WINO_TUNE_FFT;
 
 bool mask_ok(unsigned c) { return (c & ~kAllBits) == 0 && (c & (kMBits | WINO_TUNE_FFT)) != 0; }
 
-bool choice_ok(unsigned c, int m, int algo) {
-    if (algo == WINO_ALGO_FFT) return m == 14 && (c & WINO_TUNE_FFT) != 0;
+bool choice_ok(unsigned c, int m, int algo, int R, int kit) {
+    if (algo == WINO_ALGO_FFT) return m == 14 && (c & WINO_TUNE_FFT) != 0 && R == 0 && kit == 0;
     if (m != 2 && m != 4 && m != 5 && m != 6) return false;
     if (!(c & (1u << m))) return false;
-    if (algo == WINO_ALGO_THREE_STAGE) return (c & WINO_TUNE_THREE_STAGE) != 0;
-    return algo == WINO_ALGO_FUSED;
+    if (algo == WINO_ALGO_THREE_STAGE) return (c & WINO_TUNE_THREE_STAGE) != 0 && R == 0 && kit == 0;
+    return algo == WINO_ALGO_FUSED && wino::fused_blocking_built(m, R, kit);
+}
+
+// The plan of a choice: the fused blocking as an override.
+wino_plan *plan_of(int N, int C, int K, int H, int W, const Choice &c) {
+    wino_tuning t{};
+    t.tiles_per_wg = c.R;
+    t.k_per_wg = c.kit;
+    return wino_conv_plan_ex(N, C, K, H, W, c.m, c.algo, c.algo == WINO_ALGO_FUSED ? &t : nullptr);
 }
 
 // Architecture name (up to the first ':' of gcnArchName) and compute units of the
@@ -131,40 +141,44 @@ wino_plan *wino_conv_plan_tuned(int N, int C, int K, int H, int W, unsigned cand
     int cus = 0;
     if (device_key(&arch, &cus) != WINO_OK) return nullptr;
     const Key key{arch, cus, N, C, K, H, W, candidates};
-    Choice best{0, 0, 0.0};
+    Choice best{0, 0, 0, 0, 0.0};
     {
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_table.find(key);
         if (it != g_table.end()) best = it->second;
     }
     if (best.m == 0) {
+        // candidates: per tile size every built fused blocking, the three-stage
+        // algorithm if asked for, and the FFT-tile algorithm if asked for
+        std::vector<Choice> cands;
+        for (int m : {2, 4, 5, 6}) {
+            if (!(candidates & (1u << m))) continue;
+            for (const wino::FusedBlocking &b : wino::kFusedBlockings)
+                if (b.m == m) cands.push_back(Choice{m, WINO_ALGO_FUSED, b.R, b.kit, 0.0});
+            if (candidates & WINO_TUNE_THREE_STAGE) cands.push_back(Choice{m, WINO_ALGO_THREE_STAGE, 0, 0, 0.0});
+        }
+        if (candidates & WINO_TUNE_FFT) cands.push_back(Choice{14, WINO_ALGO_FFT, 0, 0, 0.0});
         Buffers b;
         bool have_buffers = false;
-        for (int m : {2, 4, 5, 6, 14}) {
-            if (m == 14 ? !(candidates & WINO_TUNE_FFT) : !(candidates & (1u << m))) continue;
-            for (int algo : {WINO_ALGO_FUSED, WINO_ALGO_THREE_STAGE, WINO_ALGO_FFT}) {
-                if ((algo == WINO_ALGO_FFT) != (m == 14)) continue;
-                if (algo == WINO_ALGO_THREE_STAGE && !(candidates & WINO_TUNE_THREE_STAGE)) continue;
-                wino_plan *p = wino_conv_plan_ex(N, C, K, H, W, m, algo, nullptr);
-                if (!p) return nullptr;  // message set by the constructor
-                if (!have_buffers) {
-                    if (b.alloc((size_t)N * C * H * W, (size_t)K * C * 9, (size_t)N * K * H * W) != WINO_OK) {
-                        wino_conv_destroy(p);
-                        return nullptr;
-                    }
-                    have_buffers = true;
+        for (Choice c : cands) {
+            wino_plan *p = plan_of(N, C, K, H, W, c);
+            if (!p) return nullptr;  // message set by the constructor
+            if (!have_buffers) {
+                if (b.alloc((size_t)N * C * H * W, (size_t)K * C * 9, (size_t)N * K * H * W) != WINO_OK) {
+                    wino_conv_destroy(p);
+                    return nullptr;
                 }
-                double us = 0.0;
-                const int st = time_plan(p, b, &us);
-                wino_conv_destroy(p);
-                if (st != WINO_OK) return nullptr;
-                if (best.m == 0 || us < best.us) best = Choice{m, algo, us};
+                have_buffers = true;
             }
+            const int st = time_plan(p, b, &c.us);
+            wino_conv_destroy(p);
+            if (st != WINO_OK) return nullptr;
+            if (best.m == 0 || c.us < best.us) best = c;
         }
         std::lock_guard<std::mutex> lk(g_mu);
         g_table[key] = best;
     }
-    wino_plan *p = wino_conv_plan_ex(N, C, K, H, W, best.m, best.algo, nullptr);
+    wino_plan *p = plan_of(N, C, K, H, W, best);
     if (!p) return nullptr;
     if (chosen_m) *chosen_m = best.m;
     if (chosen_algo) *chosen_algo = best.algo;
@@ -173,8 +187,8 @@ wino_plan *wino_conv_plan_tuned(int N, int C, int K, int H, int W, unsigned cand
 }
 
 int wino_wisdom_lookup(const char *arch, int cus, int N, int C, int K, int H, int W, unsigned candidates,
-                       int *found, int *m, int *algo) {
-    if (!arch || !found || !m || !algo) {
+                       int *found, int *m, int *algo, int *tiles_per_wg, int *k_per_wg) {
+    if (!arch || !found || !m || !algo || !tiles_per_wg || !k_per_wg) {
         wino::set_error("wino_wisdom_lookup: NULL argument");
         return WINO_EINVAL;
     }
@@ -184,6 +198,8 @@ int wino_wisdom_lookup(const char *arch, int cus, int N, int C, int K, int H, in
     if (*found) {
         *m = it->second.m;
         *algo = it->second.algo;
+        *tiles_per_wg = it->second.R;
+        *k_per_wg = it->second.kit;
     }
     return WINO_OK;
 }
@@ -198,14 +214,14 @@ int wino_wisdom_save(const char *path) {
         wino::set_error("wino_wisdom_save: cannot write %s", path);
         return WINO_EINVAL;
     }
-    fprintf(f, "# winograd wisdom: arch cus N C K H W candidates m algo microseconds\n");
+    fprintf(f, "# winograd wisdom: arch cus N C K H W candidates m algo tiles_per_wg k_per_wg microseconds\n");
     {
         std::lock_guard<std::mutex> lk(g_mu);
         for (const auto &kv : g_table) {
             const Key &k = kv.first;
-            fprintf(f, "%s %d %d %d %d %d %d 0x%x %d %d %.3f\n", std::get<0>(k).c_str(), std::get<1>(k),
+            fprintf(f, "%s %d %d %d %d %d %d 0x%x %d %d %d %d %.3f\n", std::get<0>(k).c_str(), std::get<1>(k),
                     std::get<2>(k), std::get<3>(k), std::get<4>(k), std::get<5>(k), std::get<6>(k),
-                    std::get<7>(k), kv.second.m, kv.second.algo, kv.second.us);
+                    std::get<7>(k), kv.second.m, kv.second.algo, kv.second.R, kv.second.kit, kv.second.us);
         }
     }
     if (fclose(f) != 0) {
@@ -241,18 +257,18 @@ int wino_wisdom_load(const char *path) {
         while (*s == ' ' || *s == '\t') ++s;
         if (*s == '#' || *s == '\n' || *s == '\r' || *s == '\0') continue;
         char arch[64];
-        int cus, N, C, K, H, W, m, algo, used = 0;
+        int cus, N, C, K, H, W, m, algo, R, kit, used = 0;
         unsigned cand;
         double us;
-        const int n = sscanf(s, "%63s %d %d %d %d %d %d %x %d %d %lf %n", arch, &cus, &N, &C, &K, &H, &W, &cand,
-                             &m, &algo, &us, &used);
-        if (n != 11 || s[used] != '\0' || cus < 1 || N < 1 || C < 1 || K < 1 || H < 1 || W < 1 ||
-            !mask_ok(cand) || !choice_ok(cand, m, algo) || !(us >= 0.0)) {
+        const int n = sscanf(s, "%63s %d %d %d %d %d %d %x %d %d %d %d %lf %n", arch, &cus, &N, &C, &K, &H, &W,
+                             &cand, &m, &algo, &R, &kit, &us, &used);
+        if (n != 13 || s[used] != '\0' || cus < 1 || N < 1 || C < 1 || K < 1 || H < 1 || W < 1 ||
+            !mask_ok(cand) || !choice_ok(cand, m, algo, R, kit) || !(us >= 0.0)) {
             wino::set_error("wino_wisdom_load: %s:%d: malformed entry", path, lineno);
             st = WINO_EINVAL;
             break;
         }
-        entries.push_back({Key{arch, cus, N, C, K, H, W, cand}, Choice{m, algo, us}});
+        entries.push_back({Key{arch, cus, N, C, K, H, W, cand}, Choice{m, algo, R, kit, us}});
     }
     fclose(f);
     if (st != WINO_OK) return st;

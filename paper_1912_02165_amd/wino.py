@@ -13,7 +13,7 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libwino_conv.so")
 
-WINO_OK, WINO_EINVAL, WINO_EUNSUPPORTED, WINO_ENOMEM, WINO_EHIP = 0, -1, -2, -3, -4
+WINO_OK, WINO_EINVAL, WINO_EUNSUPPORTED, WINO_ENOMEM, WINO_EHIP, WINO_EKERNEL = 0, -1, -2, -3, -4, -5
 WINO_ALGO_FUSED, WINO_ALGO_THREE_STAGE, WINO_ALGO_FFT = 0, 1, 2
 WINO_BUF_WEIGHTS, WINO_BUF_INPUT, WINO_BUF_PRODUCT = 0, 1, 2
 
@@ -35,13 +35,19 @@ SIGNATURES = {
                             ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     "wino_conv_intermediate_dims": (_i, [_vp, _i, ctypes.POINTER(ctypes.c_longlong)]),
     "wino_conv_copy_intermediate": (_i, [_vp, _i, ctypes.POINTER(ctypes.c_float), ctypes.c_size_t]),
+    "wino_conv_status": (_i, [_vp]),
+    "wino_conv_debug_set_status": (_i, [_vp, ctypes.c_uint]),
+    "wino_conv_describe": (_i, [_vp, ctypes.c_char_p, ctypes.c_size_t]),
     "wino_last_error": (ctypes.c_char_p, []),
     # wino_tune.h
     "wino_conv_plan_tuned": (_vp, [_i, _i, _i, _i, _i, ctypes.c_uint, ctypes.POINTER(_i),
                                    ctypes.POINTER(_i), ctypes.POINTER(ctypes.c_double)]),
-    "wino_conv_plan_params": (_i, [_vp, ctypes.POINTER(_i), ctypes.POINTER(_i)]),
+    "wino_conv_plan_params": (_i, [_vp, ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i),
+                                   ctypes.POINTER(_i)]),
+    "wino_fused_blockings": (_i, [ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i), _i]),
     "wino_wisdom_lookup": (_i, [ctypes.c_char_p, _i, _i, _i, _i, _i, _i, ctypes.c_uint,
-                                ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i)]),
+                                ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i),
+                                ctypes.POINTER(_i), ctypes.POINTER(_i)]),
     "wino_wisdom_save": (_i, [ctypes.c_char_p]),
     "wino_wisdom_load": (_i, [ctypes.c_char_p]),
     "wino_wisdom_clear": (None, []),
@@ -53,16 +59,12 @@ WINO_TUNE_THREE_STAGE = 1 << 8
 WINO_TUNE_FFT = 1 << 9
 WINO_TUNE_ALL_M = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M5 | WINO_TUNE_M6
 
-
-WINO_SCHED_AUTO, WINO_SCHED_SHARED, WINO_SCHED_PER_WAVE = 0, 1, 2
-WINO_SCHED_SPECIALISED, WINO_SCHED_PERSISTENT = 3, 4
 WINO_MAX_CHANNEL_SPLITS = 64
 
 
 class WinoTuning(ctypes.Structure):
-    _fields_ = [("schedule", ctypes.c_int), ("k_blocks_per_wave", ctypes.c_int),
-                ("waves_per_group", ctypes.c_int), ("tile_blocks", ctypes.c_int),
-                ("channel_splits", ctypes.c_int)]
+    _fields_ = [("tiles_per_wg", ctypes.c_int), ("k_per_wg", ctypes.c_int),
+                ("c_chunk", ctypes.c_int), ("channel_splits", ctypes.c_int)]
 
 
 class WinoError(RuntimeError):
@@ -203,18 +205,45 @@ def wino_conv_plan_tuned(N, C, K, H, W, candidates=WINO_TUNE_ALL_M):
 
 
 def wino_conv_plan_params(plan):
-    """(m, algo) of a plan."""
-    m, algo = ctypes.c_int(), ctypes.c_int()
-    _check(lib().wino_conv_plan_params(plan, ctypes.byref(m), ctypes.byref(algo)))
-    return m.value, algo.value
+    """(m, algo, tiles_per_wg, k_per_wg) of a plan (the last two 0 unless fused)."""
+    m, algo, R, kit = ctypes.c_int(), ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check(lib().wino_conv_plan_params(plan, ctypes.byref(m), ctypes.byref(algo), ctypes.byref(R),
+                                       ctypes.byref(kit)))
+    return m.value, algo.value, R.value, kit.value
+
+
+def wino_fused_blockings():
+    """[(m, tiles_per_wg, k_per_wg), ...] the fused kernel is built for."""
+    n = lib().wino_fused_blockings(None, None, None, 0)
+    m, R, kit = (ctypes.c_int * n)(), (ctypes.c_int * n)(), (ctypes.c_int * n)()
+    lib().wino_fused_blockings(m, R, kit, n)
+    return [(m[i], R[i], kit[i]) for i in range(n)]
+
+
+def wino_conv_status(plan):
+    """Raises WinoError (status WINO_EKERNEL) if a kernel wait of a call since the
+    last check gave up (synchronises the device)."""
+    return _check(lib().wino_conv_status(plan))
+
+
+def wino_conv_debug_set_status(plan, word):
+    return _check(lib().wino_conv_debug_set_status(plan, word))
+
+
+def wino_conv_describe(plan):
+    buf = ctypes.create_string_buffer(512)
+    _check(lib().wino_conv_describe(plan, buf, len(buf)))
+    return buf.value.decode()
 
 
 def wino_wisdom_lookup(arch, cus, N, C, K, H, W, candidates):
-    """(m, algo) of a wisdom entry, or None."""
+    """(m, algo, tiles_per_wg, k_per_wg) of a wisdom entry, or None."""
     found, m, algo = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    R, kit = ctypes.c_int(), ctypes.c_int()
     _check(lib().wino_wisdom_lookup(arch.encode(), cus, N, C, K, H, W, candidates,
-                                    ctypes.byref(found), ctypes.byref(m), ctypes.byref(algo)))
-    return (m.value, algo.value) if found.value else None
+                                    ctypes.byref(found), ctypes.byref(m), ctypes.byref(algo),
+                                    ctypes.byref(R), ctypes.byref(kit)))
+    return (m.value, algo.value, R.value, kit.value) if found.value else None
 
 
 def wino_wisdom_save(path):
@@ -252,14 +281,44 @@ class Plan:
         p.call_us = us
         return p
 
+    def _shape(self, t, shape, name):
+        """A tensor argument must hold exactly the plan's tensor (raw addresses are
+        passed through; the library checks their allocation's extent)."""
+        if t is None or isinstance(t, int):
+            return
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name}: expected shape {tuple(shape)} for this plan, got {tuple(t.shape)}")
+
+    def _check_xy(self, x, y):
+        N, C, K, H, W = self.shape
+        self._shape(x, (N, C, H, W), "x")
+        self._shape(y, (N, K, H, W), "y")
+
     def run(self, x, w, y, stream=None):
+        N, C, K, H, W = self.shape
+        self._check_xy(x, y)
+        self._shape(w, (K, C, 3, 3), "w")
         wino_conv_run(self.handle, x, w, y, stream)
 
     def set_weights(self, w, stream=None):
+        N, C, K, H, W = self.shape
+        self._shape(w, (K, C, 3, 3), "w")
         wino_conv_set_weights(self.handle, w, stream)
 
     def run_pretransformed(self, x, y, stream=None):
+        self._check_xy(x, y)
         wino_conv_run_pretransformed(self.handle, x, y, stream)
+
+    def status(self):
+        """Raises WinoError if a kernel wait of a call since the last check gave up."""
+        wino_conv_status(self.handle)
+
+    def describe(self):
+        return wino_conv_describe(self.handle)
+
+    def params(self):
+        """(m, algo, tiles_per_wg, k_per_wg)."""
+        return wino_conv_plan_params(self.handle)
 
     def info(self):
         return wino_conv_info(self.handle)

@@ -79,7 +79,7 @@ def test_m14_is_fft_only(lib):
 
 def test_fft_refuses_channel_splits(lib):
     t = wino.WinoTuning(channel_splits=2)
-    assert "specialised" in _plan_fails(lib, 1, 8, 4, 8, 8, 14, wino.WINO_ALGO_FFT, ctypes.byref(t))
+    assert "fused algorithm only" in _plan_fails(lib, 1, 8, 4, 8, 8, 14, wino.WINO_ALGO_FFT, ctypes.byref(t))
 
 
 def test_algorithm_names():
@@ -90,29 +90,58 @@ def test_algorithm_names():
         assert re.search(r"%s = %d\b" % (name, value), hdr)
 
 
-def test_f5_only_specialised(lib):
-    """F(5) is built for the warp-specialised fused kernel only."""
-    t = wino.WinoTuning(schedule=wino.WINO_SCHED_SHARED)
-    assert "not built" in _plan_fails(lib, 1, 4, 4, 8, 8, 5, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+def test_blockings_listed_match_header(lib):
+    """wino_fused_blockings lists the blockings the header documents as built."""
+    got = wc.wino_fused_blockings()
+    assert got == [(2, 32, 64), (2, 16, 64), (2, 32, 32), (2, 16, 32), (2, 16, 16),
+                   (4, 16, 64), (4, 16, 32), (5, 16, 32), (5, 16, 16), (6, 16, 32), (6, 16, 16)]
+    with open(os.path.join(ROOT, "include", "wino_conv.h")) as f:
+        hdr = f.read()
+    for m, R, k in got:
+        assert f"({R}, {k})" in hdr
 
 
 def test_too_large(lib):
     assert "2^31" in _plan_fails(lib, 64, 512, 512, 224, 224, 4, wino.WINO_ALGO_FUSED, None)
 
 
+def test_transformed_kernels_too_large(lib):
+    """The kernels address the transformed kernels with 32-bit byte offsets: a layer
+    whose W' reaches 2^32 bytes (C = K = 4096 at F(6): 4096 * 4096 * 64 * 4 bytes) is
+    refused before any allocation instead of wrapping the offsets."""
+    assert "2^32" in _plan_fails(lib, 1, 4096, 4096, 14, 14, 6, wino.WINO_ALGO_FUSED, None)
+    assert "2^32" in _plan_fails(lib, 1, 4096, 4096, 14, 14, 6, wino.WINO_ALGO_THREE_STAGE, None)
+
+
 def test_bad_algo(lib):
     assert "unknown algorithm" in _plan_fails(lib, 1, 4, 4, 8, 8, 4, 7, None)
 
 
-def test_bad_tuning(lib):
-    t = wino.WinoTuning(schedule=wino.WINO_SCHED_PER_WAVE, k_blocks_per_wave=3)
-    assert "not built" in _plan_fails(lib, 1, 4, 4, 8, 8, 6, wino.WINO_ALGO_FUSED, ctypes.byref(t))
-    t = wino.WinoTuning(schedule=wino.WINO_SCHED_SHARED, tile_blocks=2)
-    assert "not built" in _plan_fails(lib, 1, 4, 4, 8, 8, 6, wino.WINO_ALGO_FUSED, ctypes.byref(t))
-    t = wino.WinoTuning(schedule=5)
-    assert "not built" in _plan_fails(lib, 1, 4, 4, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
-    t = wino.WinoTuning(waves_per_group=-1)
+@pytest.mark.parametrize("m, fields", [
+    (6, dict(tiles_per_wg=32)),                 # F(6) holds 16 tiles per task
+    (6, dict(k_per_wg=64)),                     # 16 x 64 x 64 results do not fit registers
+    (4, dict(k_per_wg=16)),
+    (4, dict(tiles_per_wg=32, k_per_wg=64)),
+    (2, dict(tiles_per_wg=8)),
+    (5, dict(k_per_wg=48)),
+])
+def test_bad_tuning(lib, m, fields):
+    t = wino.WinoTuning(**fields)
+    assert "not built" in _plan_fails(lib, 1, 4, 4, 8, 8, m, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+
+
+def test_bad_tuning_fields(lib):
+    t = wino.WinoTuning(k_per_wg=-1)
     assert ">= 0" in _plan_fails(lib, 1, 4, 4, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+    # a stage holds 256 / R input channels
+    t = wino.WinoTuning(c_chunk=8)
+    assert "256 / tiles_per_wg" in _plan_fails(lib, 1, 4, 4, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+    t = wino.WinoTuning(tiles_per_wg=32, c_chunk=16)
+    assert "256 / tiles_per_wg" in _plan_fails(lib, 1, 4, 4, 8, 8, 2, wino.WINO_ALGO_FUSED, ctypes.byref(t))
+    # blocking overrides are for the fused algorithm
+    t = wino.WinoTuning(k_per_wg=32)
+    assert "fused algorithm only" in _plan_fails(lib, 1, 4, 4, 8, 8, 4, wino.WINO_ALGO_THREE_STAGE,
+                                                 ctypes.byref(t))
 
 
 def test_tuning_struct_matches_header():
@@ -133,10 +162,9 @@ def test_bad_channel_splits(lib):
     assert ">= 0" in _plan_fails(lib, 1, 64, 16, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
     t = wino.WinoTuning(channel_splits=wino.WINO_MAX_CHANNEL_SPLITS + 1)
     assert "exceeds" in _plan_fails(lib, 1, 64, 16, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
-    t = wino.WinoTuning(schedule=wino.WINO_SCHED_SHARED, channel_splits=2)
-    assert "specialised" in _plan_fails(lib, 1, 64, 16, 8, 8, 4, wino.WINO_ALGO_FUSED, ctypes.byref(t))
     t = wino.WinoTuning(channel_splits=2)
-    assert "specialised" in _plan_fails(lib, 1, 64, 16, 8, 8, 4, wino.WINO_ALGO_THREE_STAGE, ctypes.byref(t))
+    assert "fused algorithm only" in _plan_fails(lib, 1, 64, 16, 8, 8, 4, wino.WINO_ALGO_THREE_STAGE,
+                                                 ctypes.byref(t))
 
 
 def test_forced_allocation_failure(lib, monkeypatch):
@@ -154,6 +182,10 @@ def test_null_plan_calls(lib):
     assert lib.wino_conv_workspace_bytes(None) == 0
     dims = (ctypes.c_longlong * 4)()
     assert lib.wino_conv_intermediate_dims(None, 0, dims) == wino.WINO_EINVAL
+    assert lib.wino_conv_status(None) == wino.WINO_EINVAL
+    assert lib.wino_conv_debug_set_status(None, 1) == wino.WINO_EINVAL
+    buf = ctypes.create_string_buffer(64)
+    assert lib.wino_conv_describe(None, buf, 64) == wino.WINO_EINVAL
     lib.wino_conv_destroy(None)
 
 
@@ -164,10 +196,11 @@ def test_python_errors_raise(lib):
 
 # ---- wisdom table (include/wino_tune.h), host only --------------------------
 
-WISDOM = """# winograd wisdom: arch cus N C K H W candidates m algo microseconds
-gfx950 256 32 64 64 224 224 0x54 4 0 417.900
-gfx950 256 64 512 512 14 14 0x154 6 1 12.500
-gfx950 256 64 128 128 28 28 0x210 14 2 321.000
+WISDOM = """# winograd wisdom: arch cus N C K H W candidates m algo tiles_per_wg k_per_wg microseconds
+gfx950 256 32 64 64 224 224 0x54 4 0 16 64 417.900
+gfx950 256 64 512 512 14 14 0x154 6 1 0 0 12.500
+gfx950 256 64 128 128 28 28 0x210 14 2 0 0 321.000
+gfx950 256 64 128 128 28 28 0x14 4 0 16 32 57.000
 """
 
 
@@ -177,10 +210,11 @@ def test_wisdom_roundtrip(lib, tmp_path):
     src = tmp_path / "in.txt"
     src.write_text(WISDOM)
     wc.wino_wisdom_load(str(src))
-    assert wc.wino_wisdom_size() == 3
-    assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (4, 0)
-    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 128, 128, 28, 28, 0x210) == (14, 2)
-    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1)
+    assert wc.wino_wisdom_size() == 4
+    assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (4, 0, 16, 64)
+    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 128, 128, 28, 28, 0x210) == (14, 2, 0, 0)
+    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1, 0, 0)
+    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 128, 128, 28, 28, 0x14) == (4, 0, 16, 32)
     # every key field matters
     assert wc.wino_wisdom_lookup("gfx942", 256, 32, 64, 64, 224, 224, 0x54) is None
     assert wc.wino_wisdom_lookup("gfx950", 304, 32, 64, 64, 224, 224, 0x54) is None
@@ -189,31 +223,35 @@ def test_wisdom_roundtrip(lib, tmp_path):
     wc.wino_wisdom_save(str(out))
     wc.wino_wisdom_clear()
     wc.wino_wisdom_load(str(out))
-    assert wc.wino_wisdom_size() == 3
-    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1)
+    assert wc.wino_wisdom_size() == 4
+    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1, 0, 0)
     lines = [l for l in out.read_text().splitlines() if not l.startswith("#")]
     assert sorted(lines) == sorted(l for l in WISDOM.splitlines() if not l.startswith("#"))
     # a later entry with the same key replaces the earlier one
     upd = tmp_path / "upd.txt"
-    upd.write_text("gfx950 256 32 64 64 224 224 0x54 2 0 500\n")
+    upd.write_text("gfx950 256 32 64 64 224 224 0x54 2 0 32 32 500\n")
     wc.wino_wisdom_load(str(upd))
-    assert wc.wino_wisdom_size() == 3
-    assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (2, 0)
+    assert wc.wino_wisdom_size() == 4
+    assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (2, 0, 32, 32)
     wc.wino_wisdom_clear()
 
 
 @pytest.mark.parametrize("line", [
-    "gfx950 256 32 64 64 224 224 0x54 4 0",             # missing field
-    "gfx950 256 32 64 64 224 224 0x54 4 0 1.0 extra",   # extra field
-    "gfx950 256 32 64 64 224 224 0x54 3 0 1.0",         # m not a tile size
-    "gfx950 256 32 64 64 224 224 0x14 6 0 1.0",         # m not among the candidates
-    "gfx950 256 32 64 64 224 224 0x54 4 1 1.0",         # three-stage not a candidate
-    "gfx950 256 32 64 64 224 224 0x2 2 0 1.0",          # mask without a tile-size bit
-    "gfx950 256 32 64 64 224 224 0x10 14 2 1.0",        # FFT not a candidate
-    "gfx950 256 32 64 64 224 224 0x210 4 2 1.0",        # FFT with m other than 14
-    "gfx950 256 32 64 64 224 224 0x210 14 0 1.0",       # m = 14 is FFT only
-    "gfx950 256 32 0 64 224 224 0x54 4 0 1.0",          # size < 1
-    "gfx950 256 32 64 64 224 224 0x54 4 0 -1",          # negative time
+    "gfx950 256 32 64 64 224 224 0x54 4 0 16 64",             # missing field
+    "gfx950 256 32 64 64 224 224 0x54 4 0 16 64 1.0 extra",   # extra field
+    "gfx950 256 32 64 64 224 224 0x54 4 0 1.0",               # old format without the blocking
+    "gfx950 256 32 64 64 224 224 0x54 3 0 16 64 1.0",         # m not a tile size
+    "gfx950 256 32 64 64 224 224 0x14 6 0 16 32 1.0",         # m not among the candidates
+    "gfx950 256 32 64 64 224 224 0x54 4 1 0 0 1.0",           # three-stage not a candidate
+    "gfx950 256 32 64 64 224 224 0x154 4 1 16 64 1.0",        # three-stage with a blocking
+    "gfx950 256 32 64 64 224 224 0x54 4 0 32 64 1.0",         # blocking not built for m = 4
+    "gfx950 256 32 64 64 224 224 0x54 6 0 16 64 1.0",         # blocking not built for m = 6
+    "gfx950 256 32 64 64 224 224 0x2 2 0 32 64 1.0",          # mask without a tile-size bit
+    "gfx950 256 32 64 64 224 224 0x10 14 2 0 0 1.0",          # FFT not a candidate
+    "gfx950 256 32 64 64 224 224 0x210 4 2 0 0 1.0",          # FFT with m other than 14
+    "gfx950 256 32 64 64 224 224 0x210 14 0 0 0 1.0",         # m = 14 is FFT only
+    "gfx950 256 32 0 64 224 224 0x54 4 0 16 64 1.0",          # size < 1
+    "gfx950 256 32 64 64 224 224 0x54 4 0 16 64 -1",          # negative time
 ])
 def test_wisdom_rejects_malformed_and_keeps_table(lib, tmp_path, line):
     wc.wino_wisdom_clear()
@@ -221,10 +259,10 @@ def test_wisdom_rejects_malformed_and_keeps_table(lib, tmp_path, line):
     good.write_text(WISDOM)
     wc.wino_wisdom_load(str(good))
     bad = tmp_path / "bad.txt"
-    bad.write_text("gfx950 256 1 1 1 1 1 0x4 2 0 1.0\n" + line + "\n")
+    bad.write_text("gfx950 256 1 1 1 1 1 0x4 2 0 32 64 1.0\n" + line + "\n")
     with pytest.raises(wc.WinoError, match=r"bad.txt:2: malformed"):
         wc.wino_wisdom_load(str(bad))
-    assert wc.wino_wisdom_size() == 3          # nothing of the bad file was merged
+    assert wc.wino_wisdom_size() == 4          # nothing of the bad file was merged
     assert wc.wino_wisdom_lookup("gfx950", 256, 1, 1, 1, 1, 1, 0x4) is None
     wc.wino_wisdom_clear()
 
@@ -248,4 +286,4 @@ def test_plan_tuned_bad_sizes(lib):
 
 
 def test_plan_params_null(lib):
-    assert lib.wino_conv_plan_params(None, None, None) == wino.WINO_EINVAL
+    assert lib.wino_conv_plan_params(None, None, None, None, None) == wino.WINO_EINVAL

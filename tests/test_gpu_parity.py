@@ -1,11 +1,18 @@
 """GPU parity: the HIP library (through the C ABI) against the CPU oracle.
 
 * small and ragged shapes (several tiles and workgroups, C and K not multiples of
-  4 or 16, images smaller than a tile) against the full fp64 direct convolution;
+  4 or 16, images smaller than a tile) against the full fp64 direct convolution,
+  for the default plan and for every fused blocking the library is built for (the
+  candidates the tuner picks from);
 * the 56x56 layer (N=1, C=K=64) in full at every m it runs with;
-* the full-size VGG/ResNet-shaped layers in the launch configuration the
-  benchmark times, on sampled output planes the oracle computes one by one;
-* both algorithms (fused and three-stage) everywhere.
+* the full-size VGG/ResNet-shaped layers, whole outputs, in the launch
+  configuration the benchmark times (the oracle is computed once per layer), for
+  both algorithms, every tile size including F(2) and F(5) (whose outputs of 128
+  MB or more are stored with the streaming cache policy), and each layer's other
+  fused blockings; the benchmark's timed path (kernels transformed ahead, then
+  run_pretransformed) bitwise equal to run;
+* NaN inputs reaching exactly the outputs the transforms connect them to;
+* the plan's status word (bounded waits) after every call, and its plumbing.
 """
 
 import numpy as np
@@ -14,7 +21,7 @@ import torch
 
 import paper_1912_02165_amd as wc
 from paper_1912_02165_amd import workloads
-from oracle.direct import direct_conv, direct_conv_planes
+from oracle.direct import direct_conv
 from parity import assert_close
 
 pytestmark = pytest.mark.gpu
@@ -39,7 +46,7 @@ def run_gpu(x, w, m, algo, tuning=None):
     y = torch.full((N, K, H, W), float("nan"), dtype=torch.float32, device="cuda")
     with wc.Plan(N, C, K, H, W, m, algo, tuning) as p:
         p.run(xd, wd, y)
-        torch.cuda.synchronize()
+        p.status()  # synchronises; raises if a bounded wait gave up
     return y
 
 
@@ -58,6 +65,23 @@ def test_small_shapes(algo, m, shape):
     assert_close(y, direct_conv(x, w), m, f"{algo} F({m}) {shape}")
 
 
+BLOCKINGS = wc.wino_fused_blockings()
+BLOCKING_SHAPES = [(1, 1, 1, 1, 1), (1, 3, 5, 7, 9), (2, 37, 45, 29, 35), (2, 16, 33, 30, 31),
+                   (1, 130, 18, 9, 10), (1, 32, 128, 8, 8), (3, 8, 20, 17, 23), (1, 64, 64, 20, 20)]
+
+
+@pytest.mark.parametrize("blocking", BLOCKINGS, ids=lambda b: "m%d-R%d-K%d" % b)
+@pytest.mark.parametrize("shape", BLOCKING_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_every_blocking_small(blocking, shape):
+    """Every (m, tiles per task, output channels per task) the tuner may pick."""
+    m, R, kit = blocking
+    N, C, K, H, W = shape
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=sum(shape) + 3 * m + R + kit)
+    print(f"\n[gpu] blocking m={m} R={R} Kit={kit} shape={shape}", flush=True)
+    y = run_gpu(x, w, m, "fused", {"tiles_per_wg": R, "k_per_wg": kit}).cpu().numpy()
+    assert_close(y, direct_conv(x, w), m, f"F({m}) R={R} Kit={kit} {shape}")
+
+
 @pytest.mark.parametrize("algo", ALGOS)
 @pytest.mark.parametrize("m", (2, 4, 5))
 def test_layer1_full(algo, m):
@@ -69,34 +93,77 @@ def test_layer1_full(algo, m):
     print(f"rel_l2={rel:.3e} max={mx:.3e}")
 
 
-def sample_planes(N, K, seed, count=8):
-    rng = np.random.default_rng(seed)
-    planes = {(0, 0), (N - 1, K - 1), (N // 2, K // 3), (min(1, N - 1), K - 1), (N - 1, 0)}
-    while len(planes) < count:
-        planes.add((int(rng.integers(N)), int(rng.integers(K))))
-    return sorted(planes)
+_REF = {}
 
 
-# the configured pairs, plus the 14x14 C=K=512 layer at F(4) (the tile size a
-# tuned plan picks there; 4.5 rounds of work items, the last split into pieces)
-FULL_PAIRS = [(l, m) for (l, m) in workloads.PAIRS if l.id != 1] + [(workloads.LAYER_BY_ID[5], 4)]
+def layer_ref(layer):
+    """(x, w, fp64 oracle output) of a full layer, computed once per layer."""
+    if layer.id not in _REF:
+        x, w = workloads.layer_inputs(layer)
+        _REF[layer.id] = (x, w, direct_conv(x, w))
+    return _REF[layer.id]
 
 
-@pytest.mark.parametrize("algo", ALGOS)
-@pytest.mark.parametrize("pair", FULL_PAIRS, ids=lambda p: p[0].tag(p[1]))
-def test_full_layers_sampled(algo, pair):
-    layer, m = pair
-    x, w = workloads.layer_inputs(layer)
-    print(f"\n[gpu] {layer.tag(m)} {algo} full size", flush=True)
-    y = run_gpu(x, w, m, algo)
-    assert bool(torch.isfinite(y).all()), "non-finite output"
-    planes = sample_planes(layer.N, layer.K, seed=layer.id * 10 + m)
-    n_idx = torch.tensor([p[0] for p in planes], device="cuda")
-    k_idx = torch.tensor([p[1] for p in planes], device="cuda")
-    got = y[n_idx, k_idx].cpu().numpy()
-    ref = direct_conv_planes(x, w, planes)
-    rel, mx = assert_close(got, ref, m, f"{layer.tag(m)} {algo} planes {planes}")
-    print(f"rel_l2={rel:.3e} max={mx:.3e} over {len(planes)} planes")
+# (layer, m, blocking or None for the default): the configured pairs, the 14x14
+# C=K=512 layer at F(4) (the tile size the tuner picks there), F(2) and F(5) on
+# every full layer (F(2) and F(5) outputs of 128 MB or more take the streaming
+# stores), and each configured pair's other built blockings.  Grouped by layer
+# so the oracle output is computed once per layer.
+def _full_cases():
+    cases = []
+    for layer in workloads.LAYERS:
+        if layer.id == 1:
+            continue
+        ms = sorted(set(layer.ms) | {2, 4, 5} | ({6} if layer.id in (3, 5) else set()))
+        for m in ms:
+            cases.append((layer, m, None))
+            if m in layer.ms or (layer.id == 5 and m == 4):
+                for (bm, R, kit) in BLOCKINGS:
+                    if bm == m:
+                        cases.append((layer, m, (R, kit)))
+    return cases
+
+
+FULL_CASES = _full_cases()
+
+
+def _case_id(c):
+    layer, m, b = c
+    return layer.tag(m) + ("" if b is None else "-R%d-K%d" % b)
+
+
+@pytest.mark.parametrize("case", FULL_CASES, ids=_case_id)
+def test_full_layers_fused(case):
+    """Whole output of a full-size layer against the oracle; the benchmark's timed
+    path (kernels set ahead, then run_pretransformed) gives the same bits as run."""
+    layer, m, blocking = case
+    x, w, ref = layer_ref(layer)
+    tuning = None if blocking is None else {"tiles_per_wg": blocking[0], "k_per_wg": blocking[1]}
+    N, C, K, H, W = layer.N, layer.C, layer.K, layer.H, layer.W
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    y = torch.full((N, K, H, W), float("nan"), device="cuda")
+    with wc.Plan(N, C, K, H, W, m, "fused", tuning) as p:
+        print(f"\n[gpu] {_case_id(case)} fused full size: {p.describe()}", flush=True)
+        p.run(xd, wd, y)
+        p.status()
+        y2 = torch.full_like(y, float("nan"))
+        p.set_weights(wd)
+        p.run_pretransformed(xd, y2)
+        p.status()
+    assert torch.equal(y, y2), "run_pretransformed differs from run"
+    del y2
+    rel, mx = assert_close(y.cpu().numpy(), ref, m, f"{_case_id(case)} fused")
+    print(f"rel_l2={rel:.3e} max={mx:.3e} (whole output)")
+
+
+@pytest.mark.parametrize("case", [c for c in FULL_CASES if c[2] is None], ids=_case_id)
+def test_full_layers_three_stage(case):
+    layer, m, _ = case
+    x, w, ref = layer_ref(layer)
+    print(f"\n[gpu] {_case_id(case)} three_stage full size", flush=True)
+    y = run_gpu(x, w, m, "three_stage")
+    rel, mx = assert_close(y.cpu().numpy(), ref, m, f"{_case_id(case)} three_stage")
+    print(f"rel_l2={rel:.3e} max={mx:.3e} (whole output)")
 
 
 @pytest.mark.parametrize("m", (2, 4, 5, 6))
@@ -184,36 +251,25 @@ def test_guard_regions_untouched(algo):
 
 
 @pytest.mark.parametrize("algo", ALGOS)
-def test_pretransformed_matches_run(algo):
+@pytest.mark.parametrize("m", (2, 4, 5, 6))
+def test_pretransformed_matches_run(algo, m):
+    """Kernels transformed ahead (set_weights) then run_pretransformed: the same bits
+    as run, and within tolerance of the oracle."""
     N, C, K, H, W = 2, 20, 36, 15, 16
-    x, w = workloads.random_inputs(N, C, K, H, W, seed=7)
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=7 + m)
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
-    y1 = torch.empty((N, K, H, W), device="cuda")
-    y2 = torch.empty_like(y1)
-    with wc.Plan(N, C, K, H, W, 6, algo) as p:
+    y1 = torch.full((N, K, H, W), float("nan"), device="cuda")
+    y2 = torch.full_like(y1, float("nan"))
+    with wc.Plan(N, C, K, H, W, m, algo) as p:
         with pytest.raises(wc.WinoError):
             p.run_pretransformed(xd, y2)       # no kernels set yet
-        p.run(xd, wd, y1)
         p.set_weights(wd)
         p.run_pretransformed(xd, y2)
-        torch.cuda.synchronize()
+        p.status()
+        p.run(xd, wd, y1)
+        p.status()
     assert torch.equal(y1, y2)
-
-
-def test_tuning_overrides_agree():
-    x, w = workloads.random_inputs(2, 24, 64, 21, 19, seed=8)
-    ref = direct_conv(x, w)
-    for m, nkbs in ((2, (1, 2, 4)), (4, (1, 2)), (6, (1,))):
-        for nkb in nkbs:
-            for waves in (1, 2, 4):
-                t = {"schedule": wc.WINO_SCHED_PER_WAVE, "k_blocks_per_wave": nkb,
-                     "waves_per_group": waves}
-                y = run_gpu(x, w, m, "fused", t)
-                assert_close(y.cpu().numpy(), ref, m, f"per-wave F({m}) nkb={nkb} waves={waves}")
-        for tb in ((1, 2) if m <= 4 else (1,)):
-            t = {"schedule": wc.WINO_SCHED_SHARED, "tile_blocks": tb}
-            y = run_gpu(x, w, m, "fused", t)
-            assert_close(y.cpu().numpy(), ref, m, f"shared F({m}) tile_blocks={tb}")
+    assert_close(y2.cpu().numpy(), direct_conv(x, w), m, f"pretransformed {algo} F({m})")
 
 
 CSPLIT_SHAPES = [(1, 1, 1, 1, 1), (3, 8, 20, 17, 23), (2, 37, 45, 29, 35), (1, 64, 64, 20, 20),
@@ -238,20 +294,14 @@ CSPLIT_FULL = [(5, 6, 2), (5, 6, 4), (5, 4, 3), (4, 4, 2)]
 
 
 @pytest.mark.parametrize("case", CSPLIT_FULL, ids=lambda c: f"layer{c[0]}-F{c[1]}-split{c[2]}")
-def test_channel_split_full_layers_sampled(case):
+def test_channel_split_full_layers(case):
     lid, m, csplit = case
     layer = workloads.LAYER_BY_ID[lid]
-    x, w = workloads.layer_inputs(layer)
+    x, w, ref = layer_ref(layer)
     print(f"\n[gpu] {layer.tag(m)} channel split {csplit} full size", flush=True)
     y = run_gpu(x, w, m, "fused", {"channel_splits": csplit})
-    assert bool(torch.isfinite(y).all()), "non-finite output"
-    planes = sample_planes(layer.N, layer.K, seed=layer.id * 10 + m + 100 * csplit)
-    n_idx = torch.tensor([p[0] for p in planes], device="cuda")
-    k_idx = torch.tensor([p[1] for p in planes], device="cuda")
-    got = y[n_idx, k_idx].cpu().numpy()
-    ref = direct_conv_planes(x, w, planes)
-    rel, mx = assert_close(got, ref, m, f"{layer.tag(m)} channel_splits={csplit} planes {planes}")
-    print(f"rel_l2={rel:.3e} max={mx:.3e} over {len(planes)} planes")
+    rel, mx = assert_close(y.cpu().numpy(), ref, m, f"{layer.tag(m)} channel_splits={csplit}")
+    print(f"rel_l2={rel:.3e} max={mx:.3e} (whole output)")
 
 
 def test_channel_split_reproducible():
@@ -338,7 +388,11 @@ def test_plan_tuned(mask, tmp_path):
     else:
         assert mask & (1 << p.m)
         assert p.algo == "fused" or mask & wc.WINO_TUNE_THREE_STAGE
-    assert wc.wino_conv_plan_params(p.handle) == (p.m, wc.ALGOS[p.algo])
+    pm, palgo, R, kit = wc.wino_conv_plan_params(p.handle)
+    assert (pm, palgo) == (p.m, wc.ALGOS[p.algo])
+    assert (R, kit) == ((0, 0) if p.algo != "fused" else (R, kit))
+    if p.algo == "fused":
+        assert (p.m, R, kit) in BLOCKINGS
     assert p.call_us > 0
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
     y = torch.full((N, K, H, W), float("nan"), device="cuda")
@@ -346,15 +400,127 @@ def test_plan_tuned(mask, tmp_path):
     torch.cuda.synchronize()
     assert_close(y.cpu().numpy(), direct_conv(x, w), p.m, f"tuned F({p.m}) {p.algo}")
     arch, cus = _device_key()
-    assert wc.wino_wisdom_lookup(arch, cus, N, C, K, H, W, mask) == (p.m, wc.ALGOS[p.algo])
+    assert wc.wino_wisdom_lookup(arch, cus, N, C, K, H, W, mask) == (p.m, wc.ALGOS[p.algo], R, kit)
     p2 = wc.Plan.tuned(N, C, K, H, W, mask)
     assert (p2.m, p2.algo, p2.call_us) == (p.m, p.algo, p.call_us)
+    assert p2.params() == p.params()
     f = tmp_path / "wisdom.txt"
     wc.wino_wisdom_save(str(f))
     wc.wino_wisdom_clear()
     wc.wino_wisdom_load(str(f))
     p3 = wc.Plan.tuned(N, C, K, H, W, mask)
     assert (p3.m, p3.algo) == (p.m, p.algo) and abs(p3.call_us - p.call_us) < 1e-3
+    assert p3.params() == p.params()
     for q in (p, p2, p3):
         q.close()
     wc.wino_wisdom_clear()
+
+
+# ---- status word, shape checks ---------------------------------------------
+
+def test_status_word_plumbing():
+    """A bit set in the plan's status word (as a kernel wait that gave up would set
+    it) is reported once by wino_conv_status and then cleared; the plan still
+    computes correct results afterwards.  No kernel is made to give up."""
+    N, C, K, H, W = 1, 40, 48, 17, 19
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=11)
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    y = torch.full((N, K, H, W), float("nan"), device="cuda")
+    with wc.Plan(N, C, K, H, W, 4) as p:
+        p.status()
+        wc.wino_conv_debug_set_status(p.handle, 1)
+        with pytest.raises(wc.WinoError, match="gave up") as e:
+            p.status()
+        assert e.value.status == wc.WINO_EKERNEL
+        p.status()  # cleared
+        p.run(xd, wd, y)
+        p.status()
+    assert_close(y.cpu().numpy(), direct_conv(x, w), 4, "after a status reset")
+
+
+def test_wrong_shapes_refused():
+    """Tensors that do not hold the plan's tensors are refused before any launch."""
+    N, C, K, H, W = 2, 8, 24, 9, 14
+    x = torch.zeros((N, C, H, W), device="cuda")
+    w = torch.zeros((K, C, 3, 3), device="cuda")
+    y = torch.full((N, K, H, W), 7.0, device="cuda")
+    with wc.Plan(N, C, K, H, W, 4) as p:
+        with pytest.raises(ValueError, match="y: expected shape"):
+            p.run(x, w, torch.zeros((N, K - 1, H, W), device="cuda"))
+        with pytest.raises(ValueError, match="x: expected shape"):
+            p.run(torch.zeros((N, C, H + 1, W), device="cuda"), w, y)
+        with pytest.raises(ValueError, match="w: expected shape"):
+            p.set_weights(torch.zeros((K, C + 1, 3, 3), device="cuda"))
+        with pytest.raises(ValueError, match="y: expected shape"):
+            p.run_pretransformed(x, torch.zeros((N, K, H, W - 1), device="cuda"))
+        torch.cuda.synchronize()
+    assert bool((y == 7.0).all())
+
+
+# ---- non-finite inputs -----------------------------------------------------
+
+def _nan_mask(N, K, H, W, m, nan_pixels):
+    """Outputs that a NaN input reaches: output (i, j) of a tile depends on window
+    element (a, b) when the transforms connect them structurally, i.e. (|A^T| |B^T|)
+    is nonzero at (i, a) and at (j, b), from the oracle's exact matrices (for FFT
+    tiles every output of the tile depends on every window element).  The kernels
+    skip structurally zero coefficients, so exactly these outputs become NaN."""
+    from oracle import toom_cook
+    if m == 14:
+        T = 16
+        dep = np.ones((m, T), dtype=bool)
+    else:
+        AT, _, BT = toom_cook.matrices_f64(m)
+        T = m + 2
+        dep = (np.abs(np.array(AT, dtype=np.float64)) @ np.abs(np.array(BT, dtype=np.float64))) > 0
+    mask = np.zeros((N, K, H, W), dtype=bool)
+    for (n, c, h, v) in nan_pixels:
+        for ty in range((H + m - 1) // m):
+            a = h - (ty * m - 1)
+            if not 0 <= a < T:
+                continue
+            for tx in range((W + m - 1) // m):
+                b = v - (tx * m - 1)
+                if not 0 <= b < T:
+                    continue
+                for i in range(m):
+                    for j in range(m):
+                        hh, vv = ty * m + i, tx * m + j
+                        if hh < H and vv < W and dep[i, a] and dep[j, b]:
+                            mask[n, :, hh, vv] = True
+    return mask
+
+
+NAN_CASES = [(m, algo) for m in (2, 4, 5, 6) for algo in ALGOS] + [(14, "fft")]
+
+
+@pytest.mark.parametrize("case", NAN_CASES, ids=lambda c: f"m{c[0]}-{c[1]}")
+def test_nan_reaches_exactly_its_tiles(case):
+    """NaNs in x (Sec. 2.1's overlapping windows): one where a 16-tile lane row of the
+    producers wraps from one tile row to the next (the halo exchange between lanes
+    must not carry it into the previous row's last tile), one on the right and
+    bottom image edges, one on an inner tile boundary.  NaN appears exactly in the
+    outputs the transforms connect it to; every other output is finite and matches
+    the oracle."""
+    m, algo = case
+    N, C, K, H, W = 2, 20, 24, 31, 30
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=31 + m)
+    TW = (W + m - 1) // m
+    row2 = 2 * m + 1                           # a row of the third tile row
+    pixels = [(0, 3, min(row2, H - 1), 0),      # first column: left halo of tile column 0 only
+              (1, C - 1, H - 1, W - 1),         # bottom-right corner
+              (1, 0, 5, min(W - 1, (TW // 2) * m - 1))]  # last own column of an inner tile column
+    for (n, c, h, v) in pixels:
+        x[n, c, h, v] = np.nan
+    mask = _nan_mask(N, K, H, W, m, pixels)
+    print(f"\n[gpu] NaN injection {algo} m={m}: {int(mask.sum())} NaN outputs expected", flush=True)
+    y = run_gpu(x, w, m, algo).cpu().numpy()
+    got = np.isnan(y)
+    assert np.array_equal(got, mask), (f"NaN outputs: {int(got.sum())} got, {int(mask.sum())} expected, "
+                                       f"{int((got & ~mask).sum())} unexpected, {int((mask & ~got).sum())} missing")
+    assert np.isfinite(y[~mask]).all()
+    ref = direct_conv(np.nan_to_num(x, nan=0.0), w)
+    tol_m = m if m != 14 else 14
+    rel, mx = __import__("parity").errors(y[~mask], ref[~mask])
+    from parity import REL_L2, MAX_ERR
+    assert rel <= REL_L2[tol_m] and mx <= MAX_ERR, (rel, mx)
