@@ -151,6 +151,31 @@ int wino_conv_set_weights(wino_plan *p, const float *w, void *stream);
  * Returns WINO_EINVAL if the plan holds no kernels yet, otherwise as wino_conv_run. */
 int wino_conv_run_pretransformed(const wino_plan *p, const float *x, float *y, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): y = conv(x, w) as
+ * wino_conv_run does it with a fused plan of automatic blocking (kernel transform,
+ * then the fused kernel; the same kernels, so the same bits), without a plan and
+ * without allocating.  The scratch the fused path needs -- the transformed
+ * kernels (T^2 * C * K floats rounded up to the blocking), the split items'
+ * partial outputs and arrival counters -- lives in a file-scope device array of
+ * WINO_NOALLOC_SCRATCH_BYTES, one per GPU, held until the process ends; the
+ * counters are cleared by the kernel transform at every call (no memset).
+ * Every call on a GPU shares that GPU's array and leaves its own contents in it:
+ * calls that overlap on one GPU (different streams or threads) race and give
+ * wrong results; order them on one stream.  Layers whose scratch exceeds the
+ * array (for example C = K = 512 at F(6x6,3x3): 67 MB of transformed kernels)
+ * return WINO_EUNSUPPORTED before any HIP call when the transformed kernels alone
+ * do not fit, otherwise before any launch; use a plan for them.
+ * x, w, y as for wino_conv_run (device pointers on the current device).  status:
+ * NULL, or a device word into which the fused kernel ORs the bits of a bounded
+ * wait that gave up (as wino_conv_status reports them for plans; never cleared
+ * here, so a caller can check it after many calls).  Asynchronous on stream.
+ * Returns WINO_OK, WINO_EINVAL (bad sizes, m, pointer or stream),
+ * WINO_EUNSUPPORTED (too large), WINO_EHIP (a HIP call or launch failed). */
+#define WINO_NOALLOC_SCRATCH_BYTES (16u << 20)
+int wino_conv_run_noalloc(int N, int C, int K, int H, int W, int m, const float *x, const float *w,
+                          float *y, unsigned *status, void *stream);
+
 /* Free the plan and its device memory.  NULL is ignored.  The caller must make
  * sure no queued work still uses the plan. */
 void wino_conv_destroy(wino_plan *p);

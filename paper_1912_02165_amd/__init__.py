@@ -12,7 +12,7 @@ from .wino import (  # noqa: F401
     WINO_EKERNEL, WINO_MAX_CHANNEL_SPLITS,
     wino_conv_copy_intermediate, wino_conv_debug_set_status, wino_conv_describe, wino_conv_destroy,
     wino_conv_info, wino_conv_intermediate_dims, wino_conv_plan, wino_conv_plan_ex, wino_conv_run,
-    wino_conv_run_pretransformed, wino_conv_set_weights, wino_conv_status, wino_conv_workspace_bytes,
+    wino_conv_run_noalloc, wino_conv_run_pretransformed, wino_conv_set_weights, wino_conv_status, wino_conv_workspace_bytes,
     wino_last_error, wino_fused_blockings,
     WINO_TUNE_ALL_M, WINO_TUNE_M2, WINO_TUNE_M4, WINO_TUNE_M5, WINO_TUNE_M6, WINO_TUNE_THREE_STAGE, WINO_TUNE_FFT,
     wino_conv_plan_params, wino_conv_plan_tuned, wino_wisdom_clear, wino_wisdom_load,

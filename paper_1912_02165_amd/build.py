@@ -20,7 +20,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libwino_conv.so")
 OBJDIR = os.path.join(HERE, "_build")
 SOURCES = [os.path.join(CSRC, f) for f in (
-    "wino_kernels.hip", "fft_kernels.hip", "wino_api.cpp", "wino_tune.cpp")]
+    "wino_kernels.hip", "fft_kernels.hip", "wino_noalloc.hip", "wino_api.cpp", "wino_tune.cpp")]
 INST = os.path.join(CSRC, "wino_fused_inst.hip")
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Werror=return-type",

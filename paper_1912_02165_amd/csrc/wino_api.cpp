@@ -53,10 +53,12 @@ int hip_fail(const char *what, hipError_t e) {
     return WINO_EHIP;
 }
 
+}  // namespace
+
 // 64-bit geometry with overflow checks; fills g on success.
 // Tiles of edge T = m + 2 (Winograd) or T = 16, m = 14 (FFT, whose T2 counts
 // the 16 x 9 kept frequencies of a tile's half spectrum).
-int make_geometry(int N, int C, int K, int H, int W, int m, int algo, Geometry *g) {
+int wino::make_geometry(int N, int C, int K, int H, int W, int m, int algo, Geometry *g) {
     if (N < 1 || C < 1 || K < 1 || H < 1 || W < 1) {
         set_err("sizes must be >= 1 (N=%d C=%d K=%d H=%d W=%d)", N, C, K, H, W);
         return WINO_EINVAL;
@@ -91,13 +93,17 @@ int make_geometry(int N, int C, int K, int H, int W, int m, int algo, Geometry *
     return WINO_OK;
 }
 
+namespace {
+
 bool fail_alloc_forced() {
     const char *e = getenv("WINO_TEST_FAIL_ALLOC");
     return e && e[0] == '1';
 }
 
+}  // namespace
+
 // Checks that p (bytes long) is a device allocation on `device` that holds it.
-int check_device_ptr(const void *p, size_t bytes, int device, const char *name) {
+int wino::check_device_ptr(const void *p, size_t bytes, int device, const char *name) {
     if (!p) {
         set_err("%s is NULL", name);
         return WINO_EINVAL;
@@ -138,12 +144,12 @@ int check_device_ptr(const void *p, size_t bytes, int device, const char *name) 
     return WINO_OK;
 }
 
-bool overlap(const void *a, size_t na, const void *b, size_t nb) {
+bool wino::overlap(const void *a, size_t na, const void *b, size_t nb) {
     const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
     return x < y + nb && y < x + na;
 }
 
-int check_stream(const wino_plan *p, hipStream_t s) {
+int wino::check_stream_device(hipStream_t s, int device) {
     if (!s) return WINO_OK;  // null stream of the current device
     hipDevice_t dev = -1;
     hipError_t e = hipStreamGetDevice(s, &dev);
@@ -152,12 +158,20 @@ int check_stream(const wino_plan *p, hipStream_t s) {
         set_err("invalid stream (%s)", hipGetErrorString(e));
         return WINO_EINVAL;
     }
-    if (dev != p->device) {
-        set_err("stream is on device %d, the plan on device %d", dev, p->device);
+    if (dev != device) {
+        set_err("stream is on device %d, the plan on device %d", dev, device);
         return WINO_EINVAL;
     }
     return WINO_OK;
 }
+
+namespace {
+
+using wino::check_device_ptr;
+using wino::make_geometry;
+using wino::overlap;
+
+int check_stream(const wino_plan *p, hipStream_t s) { return wino::check_stream_device(s, p->device); }
 
 size_t x_bytes(const Geometry &g) { return (size_t)g.N * g.C * g.H * g.W * 4; }
 size_t y_bytes(const Geometry &g) { return (size_t)g.N * g.K * g.H * g.W * 4; }

@@ -72,8 +72,11 @@ SplitInfo fused_split_info(const Geometry &g, const FusedCfg &cfg);
 // One line naming the fused kernel a call launches and its blocking.
 void describe_fused(const Geometry &g, const FusedCfg &cfg, char *buf, size_t len);
 
-// Kernel transform: w (K x C x 3 x 3) -> wt in matrix-core operand order.
-hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt, hipStream_t s);
+// Kernel transform: w (K x C x 3 x 3) -> wt in matrix-core operand order.  The
+// first workgroup also sets the nzero words at zero to 0 (counters a following
+// fused kernel needs cleared, without a memset).
+hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt, hipStream_t s,
+                                   unsigned *zero = nullptr, int nzero = 0);
 
 // Fused: x -> y with the transformed kernels wt.
 hipError_t launch_fused(const Geometry &g, const FusedCfg &cfg, const float *x, const float *wt,
@@ -91,6 +94,15 @@ hipError_t launch_fft_fused(const Geometry &g, const float *x, const float *wt, 
 
 // Sets the message wino_last_error() returns on the calling thread (printf format).
 void set_error(const char *fmt, ...);
+
+// Host-side checks shared by the entry points (wino_api.cpp): geometry of a
+// problem with overflow checks (WINO_OK or a WINO_E* status, message set); p
+// (bytes long) a device allocation on `device` that holds it; a stream of
+// `device` (NULL: the null stream); byte ranges overlapping.
+int make_geometry(int N, int C, int K, int H, int W, int m, int algo, Geometry *g);
+int check_device_ptr(const void *p, size_t bytes, int device, const char *name);
+int check_stream_device(hipStream_t s, int device);
+bool overlap(const void *a, size_t na, const void *b, size_t nb);
 
 // Default blocking of a layer among the built ones (restricted to tiles per item
 // want_R and output channels per item want_kit where those are nonzero).

@@ -67,8 +67,11 @@ struct TileLoader {
 // >= C, output channels >= K and frequencies >= T^2 are stored as zeros.
 template <int M>
 __global__ void __launch_bounds__(256) weight_transform_kernel(const float *__restrict__ w,
-                                                               floatx4 *__restrict__ wt, Geometry g) {
+                                                               floatx4 *__restrict__ wt, Geometry g,
+                                                               unsigned *zero, int nzero) {
     constexpr int T = M + 2, T2 = T * T;
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < nzero; i += blockDim.x) zero[i] = 0u;
     const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     const long long total = (long long)g.Kb_alloc * g.Cs * 64;
     if (gid >= total) return;
@@ -211,11 +214,12 @@ __global__ void __launch_bounds__(256) output_transform_kernel(const float *__re
         default: return hipErrorInvalidValue; \
     }
 
-hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt, hipStream_t s) {
+hipError_t launch_weight_transform(const Geometry &g, const float *w, float *wt, hipStream_t s,
+                                   unsigned *zero, int nzero) {
     const long long total = (long long)g.Kb_alloc * g.Cs * 64;
     dim3 block(256), grid((unsigned)((total + 255) / 256));
     WINO_DISPATCH_M(g.m, hipLaunchKernelGGL(weight_transform_kernel<MM>, grid, block, 0, s, w,
-                                            reinterpret_cast<floatx4 *>(wt), g));
+                                            reinterpret_cast<floatx4 *>(wt), g, zero, nzero));
     return hipGetLastError();
 }
 

@@ -29,6 +29,7 @@ SIGNATURES = {
     "wino_conv_run": (_i, [_vp, _vp, _vp, _vp, _vp]),
     "wino_conv_set_weights": (_i, [_vp, _vp, _vp]),
     "wino_conv_run_pretransformed": (_i, [_vp, _vp, _vp, _vp]),
+    "wino_conv_run_noalloc": (_i, [_i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp]),
     "wino_conv_destroy": (None, [_vp]),
     "wino_conv_workspace_bytes": (ctypes.c_size_t, [_vp]),
     "wino_conv_info": (_i, [_vp, ctypes.POINTER(ctypes.c_longlong),
@@ -161,6 +162,17 @@ def wino_conv_set_weights(plan, w, stream=None):
 def wino_conv_run_pretransformed(plan, x, y, stream=None):
     return _check(lib().wino_conv_run_pretransformed(plan, _ptr(x, "x"), _ptr(y, "y"),
                                                      _stream(stream)))
+
+
+def wino_conv_run_noalloc(N, C, K, H, W, m, x, w, y, status=None, stream=None):
+    """y = conv(x, w) through the fused path without a plan and without allocating
+    (scratch in a fixed device array per GPU; calls overlapping on one GPU race).
+    status: None or a device int32/uint32 word the kernels OR their give-up bits into."""
+    st = None
+    if status is not None:
+        st = status if isinstance(status, int) else status.data_ptr()
+    return _check(lib().wino_conv_run_noalloc(N, C, K, H, W, m, _ptr(x, "x"), _ptr(w, "w"),
+                                              _ptr(y, "y"), st, _stream(stream)))
 
 
 def wino_conv_destroy(plan):

@@ -287,3 +287,16 @@ def test_plan_tuned_bad_sizes(lib):
 
 def test_plan_params_null(lib):
     assert lib.wino_conv_plan_params(None, None, None, None, None) == wino.WINO_EINVAL
+
+
+def test_noalloc_checks_before_any_hip_call(lib):
+    """wino_conv_run_noalloc refuses a bad tile size and a layer whose transformed
+    kernels exceed its scratch array (C = K = 512 at F(6x6,3x3): 67 MB) before any
+    HIP call."""
+    assert lib.wino_conv_run_noalloc(1, 4, 4, 8, 8, 3, None, None, None, None, None) == wino.WINO_EINVAL
+    assert "only F(2x2" in wc.wino_last_error()
+    rc = lib.wino_conv_run_noalloc(64, 512, 512, 14, 14, 6, None, None, None, None, None)
+    assert rc == wino.WINO_EUNSUPPORTED
+    assert "scratch" in wc.wino_last_error()
+    with open(os.path.join(ROOT, "include", "wino_conv.h")) as f:
+        assert re.search(r"#define WINO_NOALLOC_SCRATCH_BYTES \(16u << 20\)", f.read())
