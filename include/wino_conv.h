@@ -100,10 +100,11 @@ enum {
  *                   (results do not depend on the order pieces run in, but differ
  *                   from the unsplit sum by rounding).  0 or 1: no split; at most
  *                   WINO_MAX_CHANNEL_SPLITS.
- * Automatic choice (wino_conv_plan): the largest R and k that fit (most reuse of
- * each transformed input tile and transformed-kernel operand), unless a
- * smaller k fills the compute units with enough more work items to be
- * estimated at least 10 % faster; wino_conv_plan_tuned measures instead. */
+ * Automatic choice (wino_conv_plan): the largest task that fits (k at its
+ * maximum, R = 32 for m = 2 with C <= 64, else 16: most reuse of each
+ * transformed input tile and transformed-kernel operand) as long as the layer has
+ * at least one task per compute unit; otherwise the blocking with the most
+ * tasks.  wino_conv_plan_tuned measures every blocking instead. */
 #define WINO_MAX_CHANNEL_SPLITS 64
 typedef struct {
     int tiles_per_wg;
@@ -127,8 +128,8 @@ wino_plan *wino_conv_plan(int N, int C, int K, int H, int W, int m);
 /* As wino_conv_plan, choosing the algorithm (WINO_ALGO_*) and optional blocking
  * overrides (t may be NULL; they apply to WINO_ALGO_FUSED and are ignored by the
  * others, except that channel_splits > 1 is refused for them).  The
- * three-stage plan also allocates its intermediate buffers (2 * T^2 * tiles *
- * max(C, K) floats, rounded up); the FFT plan's transformed kernels take
+ * three-stage plan also allocates its intermediate buffers (T^2 * tiles * (C + K)
+ * floats, rounded up to the blocking); the FFT plan's transformed kernels take
  * 144 * 16 bytes per (input, output) channel pair, padded to multiples of 4 and
  * 16. */
 wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
@@ -203,8 +204,16 @@ int wino_conv_info(const wino_plan *p, long long *n_tiles, double *direct_flops,
  *                     column q <= 8), lane (c%4)*16 + k%16, holding {Re, Im,
  *                     -Im, 0} of the spectrum of w[k,c] zero-padded to 16 x 16;
  *                     dims returned {Cs, Kb, 144, 256}.
- *   WINO_BUF_INPUT:   [T^2][Cp][tiles_p]  (three-stage plans only)
- *   WINO_BUF_PRODUCT: [T^2][Kp][tiles_p]  (three-stage plans only)
+ *   WINO_BUF_INPUT:   three-stage plans only: [F4][TB][Cs][64][4], F4 =
+ *                     ceil(T^2/4), TB = tiles rounded up to 64, / 16: element
+ *                     (f, c, t) of U = B^T d B at f4 = f/4, tb = t/16, cs = c/4,
+ *                     lane (c%4)*16 + t%16, slot f%4.  Dims {F4, TB, Cs, 256}.
+ *   WINO_BUF_PRODUCT: three-stage plans only: [F4][TB][Kb][4][64][4], Kb =
+ *                     ceil(K/16) rounded up to 4: element (f, k, t) of
+ *                     M = sum_c W' U at f4 = f/4, tb = t/16, kb = k/16, v = k%4,
+ *                     lane ((k%16)/4)*16 + t%16, slot f%4.  Dims {F4, TB, Kb, 1024}.
+ *                     Channels, output channels, tiles and frequencies past the
+ *                     problem hold zeros.
  * Frequency f = i*T + j for transform row i, column j; tile t = (n*TH + ty)*TW + tx. */
 int wino_conv_intermediate_dims(const wino_plan *p, int which, long long dims[4]);
 

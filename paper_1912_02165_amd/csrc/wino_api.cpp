@@ -22,8 +22,8 @@ struct wino_plan {
     int device;
     float *wt;        // transformed kernels, matrix-core operand order
     size_t wt_bytes;
-    float *U;         // three-stage: transformed input  [T2][Cp][tiles_p]
-    float *Mf;        // three-stage: per-frequency sums [T2][Kp][tiles_p]
+    float *U;         // three-stage: transformed input tiles  [F4][TB][Cs][64][4]
+    float *Mf;        // three-stage: per-frequency sums       [F4][TB][Kb_alloc][4][64][4]
     size_t U_bytes, M_bytes;
     wino::SplitBuffers split;  // fused: partial outputs of split items and their counters
     size_t part_bytes, cnt_bytes;
@@ -276,8 +276,10 @@ wino_plan *wino_conv_plan_ex(int N, int C, int K, int H, int W, int m, int algo,
                                 : (size_t)g.Kb_alloc * 16 * g.Cs * 4 * ((g.T2 + 3) / 4 * 4) * sizeof(float);
     size_t U_bytes = 0, M_bytes = 0;
     if (algo == WINO_ALGO_THREE_STAGE) {
-        U_bytes = (size_t)g.T2 * g.Cs * 4 * g.tiles_p * sizeof(float);
-        M_bytes = (size_t)g.T2 * g.Kb_alloc * 16 * g.tiles_p * sizeof(float);
+        // frequencies padded to whole float4s (F(5): 49 -> 52)
+        const size_t T2p = (size_t)(g.T2 + 3) / 4 * 4;
+        U_bytes = T2p * g.Cs * 4 * g.tiles_p * sizeof(float);
+        M_bytes = T2p * g.Kb_alloc * 16 * g.tiles_p * sizeof(float);
     }
     // The kernels address the transformed kernels, the input and the output with
     // 32-bit byte offsets (buffer resources): each must stay below 2^32 bytes.
@@ -550,11 +552,11 @@ int wino_conv_intermediate_dims(const wino_plan *p, int which, long long dims[4]
             return WINO_OK;
         case WINO_BUF_INPUT:
             if (!p->U) break;
-            dims[0] = g.T2; dims[1] = (long long)g.Cs * 4; dims[2] = g.tiles_p; dims[3] = 1;
+            dims[0] = (g.T2 + 3) / 4; dims[1] = g.tiles_p / 16; dims[2] = g.Cs; dims[3] = 256;
             return WINO_OK;
         case WINO_BUF_PRODUCT:
             if (!p->Mf) break;
-            dims[0] = g.T2; dims[1] = (long long)g.Kb_alloc * 16; dims[2] = g.tiles_p; dims[3] = 1;
+            dims[0] = (g.T2 + 3) / 4; dims[1] = g.tiles_p / 16; dims[2] = g.Kb_alloc; dims[3] = 1024;
             return WINO_OK;
         default:
             break;

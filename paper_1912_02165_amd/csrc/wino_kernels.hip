@@ -16,49 +16,6 @@ namespace wino {
 WINO_FUSED_BLOCKINGS(WINO_EXTERN_WS)
 #undef WINO_EXTERN_WS
 
-// Load the T x T input tile of (tile, channel c) with implicit zero padding
-// (Sec. 2.1): rows ty*M - 1 + a, columns tx*M - 1 + b.  Reads use clamped,
-// always in-bounds addresses; out-of-image elements are then replaced by 0.
-template <int M>
-struct TileLoader {
-    static constexpr int T = M + 2;
-    int rowoff[T];
-    int colc[T];
-    unsigned rowok;  // bit a: row a inside the image (and the tile exists)
-    unsigned colok;  // bit b: column b inside the image
-
-    __device__ __forceinline__ void init(const Geometry &g, const TileIdx &t) {
-        rowok = 0u;
-        colok = 0u;
-#pragma unroll
-        for (int a = 0; a < T; ++a) {
-            int h = t.ty * M - 1 + a;
-            if (t.ok && h >= 0 && h < g.H) rowok |= 1u << a;
-            rowoff[a] = clampi(h, 0, g.H - 1) * g.W;
-        }
-#pragma unroll
-        for (int b = 0; b < T; ++b) {
-            int w = t.tx * M - 1 + b;
-            if (w >= 0 && w < g.W) colok |= 1u << b;
-            colc[b] = clampi(w, 0, g.W - 1);
-        }
-    }
-
-    // xc points at channel plane (n, c); cok says whether c < C.
-    __device__ __forceinline__ void load(const float *__restrict__ xc, bool cok, float *d) const {
-#pragma unroll
-        for (int a = 0; a < T; ++a) {
-            const float *xr = xc + rowoff[a];
-            bool rok = cok && ((rowok >> a) & 1u);
-#pragma unroll
-            for (int b = 0; b < T; ++b) {
-                float v = xr[colc[b]];
-                d[a * T + b] = (rok && ((colok >> b) & 1u)) ? v : 0.0f;
-            }
-        }
-    }
-};
-
 // ---------------------------------------------------------------------------
 // Kernel transform (Sec. 3, step 2: right-hand matrices transformed ahead of
 // time).  Thread (kb, cs, lane) transforms kernel (k, c) with k = 16 kb + lane%16,
@@ -100,106 +57,175 @@ __global__ void __launch_bounds__(256) weight_transform_kernel(const float *__re
 }
 
 // ---------------------------------------------------------------------------
-// Three-stage pipeline (Sec. 3): stage 1 writes U[f][c][tile] for all tiles,
-// stage 2 forms M[f][k][tile] = sum_c W'[f][c][k] U[f][c][tile] for each f,
-// stage 3 inverse-transforms M into y.  Padded rows (c >= C, k >= K, tile >= ntiles)
-// of U and M hold zeros.
+// Three-stage pipeline (Sec. 3): stage 1 writes the transformed input tiles U of
+// all tiles to device memory, stage 2 forms M[f][k][tile] = sum_c W'[f][c][k]
+// U[f][c][tile] for every frequency f, stage 3 inverse-transforms M into y.
+// The intermediates are stored in the matrix-core operand order, four
+// consecutive frequencies per 16-byte element, so that every stage moves them
+// with one coalesced 1 KB access per wave and instruction:
+//   U [F4][TB][Cs][64][4]:    element (f, c, tile) at f4 = f/4, tb = tile/16,
+//                             cs = c/4, lane (c%4)*16 + tile%16, slot f%4 (the B
+//                             operand of v_mfma_f32_16x16x4f32 for 4 frequencies);
+//   M [F4][TB][Kb][4][64][4]: element (f, k, tile) at f4, tb, kb = k/16, v = k%4,
+//                             lane ((k%16)/4)*16 + tile%16, slot f%4 (the
+//                             accumulator layout: lane l holds D[4(l/16)+v][l%16]).
+// TB = tiles_p / 16, Cs = ceil(C/4), Kb = Kb_alloc; channels, output channels and
+// tiles past the problem hold zeros.
 
-template <int M>
+// Stage 1: the workgroup's 256 threads are 16 tiles x 16 channels (the producer
+// mapping of the fused kernel: lane%16 = tile, so the row-vector loader's DPP halo
+// exchange applies); each transforms its tile and stores one float4 per four
+// frequencies.
+template <int M, bool VX>
 __global__ void __launch_bounds__(256) input_transform_kernel(const float *__restrict__ x,
-                                                              float *__restrict__ U, Geometry g) {
-    constexpr int T = M + 2, T2 = T * T;
-    const int tile = blockIdx.x * blockDim.x + threadIdx.x;
-    const int c = blockIdx.y;
-    if (tile >= g.tiles_p) return;
-    const TileIdx ti = decode_tile(g, tile);
-    TileLoader<M> ld;
-    ld.init(g, ti);
+                                                              floatx4 *__restrict__ U, Geometry g) {
+    constexpr int T2 = (M + 2) * (M + 2);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int tr = tid & 15, cl = tid >> 4;
+    const int tb = blockIdx.x, c = blockIdx.y * 16 + cl;
+    const int TB = g.tiles_p / 16;
+    if (c >= g.Cs * 4) return;  // past the last 4-channel step
+    const TileIdx ti = decode_tile(g, tb * 16 + tr);
     const long long HW = (long long)g.H * g.W;
-    const bool cok = c < g.C;
+    const int32x4 rs = make_rsrc(x, (unsigned)((long long)g.N * g.C * HW * 4));
     float d[T2];
-    ld.load(x + ((long long)ti.n * g.C + (cok ? c : 0)) * HW, cok, d);
-    float u[T2];
-    input_tile_transform<M>(d, u);
-    const long long Cp = (long long)g.Cs * 4;
-#pragma unroll
-    for (int f = 0; f < T2; ++f) U[((long long)f * Cp + c) * g.tiles_p + tile] = u[f];
-}
-
-// Stage 2: per frequency f (blockIdx.z), each wave computes 64 output channels x
-// 32 tiles with 4 x 2 matrix-core blocks.
-template <int M>
-__global__ void __launch_bounds__(256) frequency_gemm_kernel(const float *__restrict__ U,
-                                                             const float *__restrict__ wt,
-                                                             float *__restrict__ Mout, Geometry g) {
-    constexpr int T = M + 2, T2 = T * T;
-    constexpr int KBW = 4, TBW = 2;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int waves = blockDim.x >> 6;
-    const int f = blockIdx.z;
-    const int t0 = (blockIdx.x * waves + wave) * (16 * TBW);
-    if (t0 >= g.tiles_p) return;
-    const int kb0 = blockIdx.y * KBW;
-    const long long Cp = (long long)g.Cs * 4;
-    const long long Kp = (long long)g.Kb_alloc * 16;
-    floatx4 acc[KBW][TBW];
-#pragma unroll
-    for (int i = 0; i < KBW; ++i)
-#pragma unroll
-        for (int j = 0; j < TBW; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const float *ub = U + ((long long)f * Cp + (lane >> 4)) * g.tiles_p + t0 + (lane & 15);
-    const float *wb = wt + (long long)(f >> 2) * 256 + lane * 4 + (f & 3);
-    for (int cs = 0; cs < g.Cs; ++cs) {
-        float a[KBW], b[TBW];
-#pragma unroll
-        for (int i = 0; i < KBW; ++i) a[i] = wb[((long long)(kb0 + i) * g.Cs + cs) * (4 * freq_quads<M>()) * 64];
-#pragma unroll
-        for (int j = 0; j < TBW; ++j) b[j] = ub[(long long)cs * 4 * g.tiles_p + j * 16];
-#pragma unroll
-        for (int i = 0; i < KBW; ++i)
-#pragma unroll
-            for (int j = 0; j < TBW; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    if constexpr (VX) {
+        RowTile<M> ld;
+        TileIdx rf, rl;
+        row_edges<1>(g, tb * 16, tr, rf, rl);
+        ld.init(g, ti, rf, rl, c, tr);
+        ld.issue(rs, d);
+        RowTile<M>::finish(d, ld.flags(), (g.W % M) != 0);
+    } else {
+        BufTile<M, (M <= 2)> ld;
+        ld.init(g, ti, c);
+        ld.load(rs, d);
     }
+    if (c >= g.C) {  // channel padding (its loads read another channel's plane)
 #pragma unroll
-    for (int i = 0; i < KBW; ++i)
-#pragma unroll
-        for (int j = 0; j < TBW; ++j)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const long long k = (kb0 + i) * 16 + (lane >> 4) * 4 + v;
-                Mout[((long long)f * Kp + k) * g.tiles_p + t0 + j * 16 + (lane & 15)] = acc[i][j][v];
-            }
+        for (int f = 0; f < T2; ++f) d[f] = 0.0f;
+    }
+    floatx4 *dst = U + ((long long)tb * g.Cs + (c >> 2)) * 64 + lane;
+    const long long fstride = (long long)TB * g.Cs * 64;
+    input_tile_transform_emit<M>(d, [&](int f4, float a, float b, float cc, float e) {
+        dst[f4 * fstride] = floatx4{a, b, cc, e};
+    });
 }
 
+// Stage 2: per workgroup four frequencies (one float4 of operands) x 4 tile blocks
+// x 4 output blocks (64 tiles x 64 output channels); each of the 4 waves
+// multiplies 2 tile blocks by 2 output blocks for the 4 frequencies (16 matrix
+// products per 4-channel step from 4 operand loads of 1 KB), operands of the next
+// step loaded during the current one.  Workgroups are numbered so that the output
+// groups of one tile group are consecutive on one XCD (workgroup b runs on XCD b %
+// 8), so the tile group's U is read from HBM once and then from that XCD's L2.
 template <int M>
-__global__ void __launch_bounds__(256) output_transform_kernel(const float *__restrict__ Min,
-                                                               float *__restrict__ y, Geometry g) {
-    constexpr int T = M + 2, T2 = T * T;
-    const int tile = blockIdx.x * blockDim.x + threadIdx.x;
-    const int k = blockIdx.y;
-    if (tile >= g.ntiles) return;
-    const TileIdx ti = decode_tile(g, tile);
-    const long long Kp = (long long)g.Kb_alloc * 16;
-    float mm[T2];
+__global__ void __launch_bounds__(256) frequency_gemm_kernel(const floatx4 *__restrict__ U,
+                                                             const floatx4 *__restrict__ wt,
+                                                             floatx4 *__restrict__ Mout, Geometry g) {
+    constexpr int Q = freq_quads<M>();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int TB = g.tiles_p / 16, TG = TB / 4, KG = g.Kb_alloc / 4;
+    const int nblk = gridDim.x;
+    // XCD-contiguous logical block index
+    const int xcd = blockIdx.x % 8, per = nblk / 8, extra = nblk % 8;
+    const int lb = xcd * per + (xcd < extra ? xcd : extra) + blockIdx.x / 8;
+    const int kg = lb % KG, rest = lb / KG;
+    const int tg = rest % TG, f4 = rest / TG;
+    const int kb0 = kg * 4 + (wave & 1) * 2, tb0 = tg * 4 + (wave >> 1) * 2;
+    const int Cs = g.Cs;
+    const floatx4 *ap = wt + ((long long)kb0 * Cs * Q + f4) * 64 + lane;       // + (i * Cs + cs) * Q * 64
+    const floatx4 *bp = U + (((long long)f4 * TB + tb0) * Cs) * 64 + lane;     // + (j * Cs + cs) * 64
+    floatx4 acc[2][2][4];
 #pragma unroll
-    for (int f = 0; f < T2; ++f) mm[f] = Min[((long long)f * Kp + k) * g.tiles_p + tile];
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) acc[i][j][q] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // Operands in flight: the transformed kernels (mostly L2 hits) one step ahead,
+    // the transformed input tiles (streamed from HBM) two steps ahead, in
+    // rotating register sets; the loop is unrolled by three so every set is
+    // named statically.  Loads past the last step are clamped to it.
+    auto loada = [&](floatx4 (&a)[2], int cs) {
+        cs = cs < Cs ? cs : Cs - 1;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) a[i] = ap[((long long)i * Cs + cs) * Q * 64];
+    };
+    auto loadb = [&](floatx4 (&b)[2], int cs) {
+        cs = cs < Cs ? cs : Cs - 1;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) b[j] = bp[((long long)j * Cs + cs) * 64];
+    };
+    auto mul = [&](const floatx4 (&a)[2], const floatx4 (&b)[2]) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j][q], 0, 0, 0);
+    };
+    floatx4 a0[2], a1[2], b0[2], b1[2], b2[2];
+    loadb(b0, 0);
+    loadb(b1, 1);
+    loada(a0, 0);
+    int cs = 0;
+    // step cs uses a(cs % 2), b(cs % 3); before it, step cs + 1's a and step
+    // cs + 2's b are issued
+    for (; cs + 6 <= Cs; cs += 6) {
+        loada(a1, cs + 1); loadb(b2, cs + 2); mul(a0, b0);
+        loada(a0, cs + 2); loadb(b0, cs + 3); mul(a1, b1);
+        loada(a1, cs + 3); loadb(b1, cs + 4); mul(a0, b2);
+        loada(a0, cs + 4); loadb(b2, cs + 5); mul(a1, b0);
+        loada(a1, cs + 5); loadb(b0, cs + 6); mul(a0, b1);
+        loada(a0, cs + 6); loadb(b1, cs + 7); mul(a1, b2);
+    }
+    // fewer than six steps left: the sets rotate as in the loop
+    if (cs < Cs) { loada(a1, cs + 1); loadb(b2, cs + 2); mul(a0, b0); }
+    if (cs + 1 < Cs) { loada(a0, cs + 2); loadb(b0, cs + 3); mul(a1, b1); }
+    if (cs + 2 < Cs) { loada(a1, cs + 3); loadb(b1, cs + 4); mul(a0, b2); }
+    if (cs + 3 < Cs) { loada(a0, cs + 4); loadb(b2, cs + 5); mul(a1, b0); }
+    if (cs + 4 < Cs) { mul(a0, b1); }
+    // M: one float4 (4 frequencies) per lane and (tile block, output block, v)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                Mout[((((long long)f4 * TB + tb0 + j) * g.Kb_alloc + kb0 + i) * 4 + v) * 64 + lane] =
+                    floatx4{acc[i][j][0][v], acc[i][j][1][v], acc[i][j][2][v], acc[i][j][3][v]};
+}
+
+// Stage 3: the workgroup's 4 waves are the four v of one (tile block, output
+// block): lane = 16 * q + tile%16 with output channel k = 16 kb + 4 q + v, so a
+// wave reads one 1 KB float4 row of M per four frequencies.
+template <int M>
+__global__ void __launch_bounds__(256) output_transform_kernel(const floatx4 *__restrict__ Min,
+                                                               float *__restrict__ y, Geometry g) {
+    constexpr int T2 = (M + 2) * (M + 2), Q = freq_quads<M>();
+    const int lane = threadIdx.x & 63, v = threadIdx.x >> 6;
+    const int tb = blockIdx.x, kb = blockIdx.y;
+    const int TB = g.tiles_p / 16;
+    const int tile = tb * 16 + (lane & 15), k = kb * 16 + (lane >> 4) * 4 + v;
+    const floatx4 *src = Min + (((long long)tb * g.Kb_alloc + kb) * 4 + v) * 64 + lane;
+    const long long fstride = (long long)TB * g.Kb_alloc * 4 * 64;
+    float mm[4 * Q];
+#pragma unroll
+    for (int f4 = 0; f4 < Q; ++f4) {
+        const floatx4 q4 = src[f4 * fstride];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mm[4 * f4 + e] = q4[e];
+    }
+    if (tile >= g.ntiles || k >= g.K) return;
+    const TileIdx ti = decode_tile(g, tile);
     float yy[M * M];
     output_tile_transform<M>(mm, yy);
-    const long long HW = (long long)g.H * g.W;
-    float *yp = y + ((long long)ti.n * g.K + k) * HW;
-#pragma unroll
-    for (int i = 0; i < M; ++i) {
-        const int h = ti.ty * M + i;
-        if (h < g.H) {
-#pragma unroll
-            for (int j = 0; j < M; ++j) {
-                const int w = ti.tx * M + j;
-                if (w < g.W) yp[(long long)h * g.W + w] = yy[i * M + j];
-            }
-        }
-    }
+    (void)T2;
+    const bool vec = (M == 4) ? (g.W % 4 == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0)
+                              : (g.W % 2 == 0 && (reinterpret_cast<uintptr_t>(y) & 7) == 0);
+    store_tile<M>(y + ((long long)ti.n * g.K + k) * g.H * g.W, yy, ti.ty * M, ti.tx * M, g, vec);
 }
 
 // ---------------------------------------------------------------------------
@@ -230,50 +256,50 @@ bool fused_blocking_built(int m, int R, int kit) {
 }
 
 // Default blocking of a layer, from the capacity bounds of Sec. 4.1 and the
-// number of work-item rounds.
+// number of work items.
 //  * Capacity: a task's result matrices (R tiles x Kit output channels x T^2
 //    frequencies) live in the consumer waves' registers, at most 144 per lane of
-//    four waves: R * Kit * T^2 <= 36864.  F(2), F(4): R = 16 or 32 with Kit <= 64;
-//    F(5), F(6): R = 16, Kit <= 32.
+//    four waves: R * Kit * T^2 <= 36864.  F(2), F(4): Kit <= 64 (R = 32 only for
+//    F(2)); F(5), F(6): R = 16, Kit <= 32.
 //  * Reuse: every transformed input tile is multiplied by the Kit output
-//    channels' kernels (the input-transform cost per product falls as 1 / Kit),
+//    channels' kernels (the input-transform work per product falls as 1 / Kit)
 //    and every transformed-kernel operand read from L2 by the R tiles (the
 //    paper's task arithmetic intensity against the shared cache, R / 2).  So the
-//    largest R and Kit that fit are preferred ...
-//  * ... unless the layer has too few items to fill the compute units: the
-//    estimated time of a blocking is its item cost (products plus input
-//    transforms, in SIMD cycles) times the rounds of items the persistent grid
-//    runs, including the split of a last, partly filled round; a smaller Kit is
-//    taken when it is estimated at least 10 % faster.
+//    largest task that fits is taken: Kit at its maximum; R = 32 for F(2) when C
+//    <= 64 (measured: with more channels the 16-channel stages of R = 16 run
+//    faster), else 16 ...
+//  * ... as long as the layer has at least one task per compute unit.  A layer
+//    with fewer takes the blocking with the most tasks instead (smaller Kit,
+//    then smaller R): on the N=1, 56x56, C=K=64 layer at F(2) 196 tasks of 16 x
+//    16 run in 8.4 us against 14.8 us for 25 tasks of 32 x 64.
+// Measured on every layer (steady state, one MI355X): splitting a task's output
+// channels among its consumer waves costs more than the transform reuse it gives
+// up whenever the larger tasks already fill the compute units.
 FusedCfg fused_cfg_default(const Geometry &g, int num_cus, int want_R, int want_kit) {
-    const int T2 = (g.m + 2) * (g.m + 2);
-    // vector instructions of one input-tile transform (B^T d B), per tile and channel
-    const double in_ops = g.m == 2 ? 32.0 : g.m == 4 ? 150.0 : g.m == 5 ? 270.0 : 390.0;
     FusedCfg best{};
-    double best_t = 0.0;
-    const int Rs[2] = {32, 16};
-    const int kits[3] = {64, 32, 16};
-    for (int R : Rs) {
-        for (int kit : kits) {
-            if (!fused_blocking_built(g.m, R, kit) || (want_R && R != want_R) || (want_kit && kit != want_kit))
-                continue;
-            FusedCfg c{R, kit, num_cus, 0};
-            const SplitInfo si = fused_split_info(g, c);
-            // SIMD cycles per item: products (32 multiply-adds per cycle) and
-            // input transforms (16 lane-operations per cycle), over 4 SIMDs
-            const double per_tc = (double)kit * T2 / 32.0 + in_ops / 16.0;
-            const double item = (double)R * g.C * per_tc / 4.0;
-            double rounds = (double)si.nfull;
-            if (si.n_tail > 0) {
-                rounds += (double)((si.n_units + num_cus - 1) / num_cus) / si.maxc;
-            } else if (si.n_items > si.nfull * num_cus) {
-                rounds += 1.0;
-            }
-            const double t = rounds * item;
-            if (best.R == 0 || t < 0.9 * best_t) {
-                best = c;
-                best_t = t;
-            }
+    int best_items = -1;
+    bool best_fills = false;
+    const int pref_R = (g.m == 2 && g.C <= 64) ? 32 : 16;
+    for (const FusedBlocking &b : kFusedBlockings) {
+        if (b.m != g.m || (want_R && b.R != want_R) || (want_kit && b.kit != want_kit)) continue;
+        const FusedCfg c{b.R, b.kit, num_cus, 0};
+        const int items = fused_split_info(g, c).n_items;
+        const bool fills = items >= num_cus;
+        bool take;
+        if (best.R == 0) take = true;
+        else if (fills != best_fills) take = fills;
+        else if (fills) {
+            // both fill the units: the largest task, R = pref_R first
+            const bool bp = best.R == pref_R, cp = b.R == pref_R;
+            take = b.kit > best.kit || (b.kit == best.kit && cp && !bp);
+        } else {
+            // neither fills the units: the most tasks
+            take = items > best_items;
+        }
+        if (take) {
+            best = c;
+            best_items = items;
+            best_fills = fills;
         }
     }
     return best;
@@ -326,24 +352,34 @@ void describe_three_stage(const Geometry &g, char *buf, size_t len) {
 }
 
 hipError_t launch_input_transform(const Geometry &g, const float *x, float *U, hipStream_t s) {
-    dim3 block(256), grid((unsigned)((g.tiles_p + 255) / 256), (unsigned)(g.Cs * 4));
-    WINO_DISPATCH_M(g.m, hipLaunchKernelGGL(input_transform_kernel<MM>, grid, block, 0, s, x, U, g));
+    dim3 block(256), grid((unsigned)(g.tiles_p / 16), (unsigned)((g.Cs * 4 + 15) / 16));
+    // row-vector input loads need every row start aligned to the vector width
+    const unsigned vw = (g.m == 4) ? 16u : (g.m == 5) ? 4u : 8u;
+    const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
+    floatx4 *u4 = reinterpret_cast<floatx4 *>(U);
+    if (vx) {
+        WINO_DISPATCH_M(g.m, hipLaunchKernelGGL((input_transform_kernel<MM, true>), grid, block, 0, s, x, u4, g));
+    } else {
+        WINO_DISPATCH_M(g.m, hipLaunchKernelGGL((input_transform_kernel<MM, false>), grid, block, 0, s, x, u4, g));
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_frequency_gemm(const Geometry &g, const float *U, const float *wt, float *Mout,
                                  hipStream_t s) {
-    const int waves = 4, tiles_per_wave = 32;
-    dim3 block(64 * waves);
-    dim3 grid((unsigned)((g.tiles_p + waves * tiles_per_wave - 1) / (waves * tiles_per_wave)),
-              (unsigned)(g.Kb_alloc / 4), (unsigned)g.T2);
-    WINO_DISPATCH_M(g.m, hipLaunchKernelGGL(frequency_gemm_kernel<MM>, grid, block, 0, s, U, wt, Mout, g));
+    const long long nblk = (long long)(g.tiles_p / 64) * (g.Kb_alloc / 4) * ((g.T2 + 3) / 4);
+    dim3 block(256), grid((unsigned)nblk);
+    WINO_DISPATCH_M(g.m, hipLaunchKernelGGL(frequency_gemm_kernel<MM>, grid, block, 0, s,
+                                            reinterpret_cast<const floatx4 *>(U),
+                                            reinterpret_cast<const floatx4 *>(wt),
+                                            reinterpret_cast<floatx4 *>(Mout), g));
     return hipGetLastError();
 }
 
 hipError_t launch_output_transform(const Geometry &g, const float *Min, float *y, hipStream_t s) {
-    dim3 block(256), grid((unsigned)((g.ntiles + 255) / 256), (unsigned)g.K);
-    WINO_DISPATCH_M(g.m, hipLaunchKernelGGL(output_transform_kernel<MM>, grid, block, 0, s, Min, y, g));
+    dim3 block(256), grid((unsigned)(g.tiles_p / 16), (unsigned)g.Kb);
+    WINO_DISPATCH_M(g.m, hipLaunchKernelGGL(output_transform_kernel<MM>, grid, block, 0, s,
+                                            reinterpret_cast<const floatx4 *>(Min), y, g));
     return hipGetLastError();
 }
 

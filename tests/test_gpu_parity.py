@@ -178,9 +178,9 @@ def test_three_stage_intermediates(m):
     with wc.Plan(N, C, K, H, W, m, "three_stage") as p:
         p.run(xd, wd, y)
         torch.cuda.synchronize()
-        wt = p.intermediate(wc.WINO_BUF_WEIGHTS)       # (Kb, Cs, T2, 64) operand order
-        U = p.intermediate(wc.WINO_BUF_INPUT)          # (T2, Cp, tiles_p, 1)
-        Mf = p.intermediate(wc.WINO_BUF_PRODUCT)       # (T2, Kp, tiles_p, 1)
+        wt = p.intermediate(wc.WINO_BUF_WEIGHTS)       # (Kb, Cs, T2P, 64) operand order
+        U = p.intermediate(wc.WINO_BUF_INPUT)          # (F4, TB, Cs, 256) operand order
+        Mf = p.intermediate(wc.WINO_BUF_PRODUCT)       # (F4, TB, Kb, 1024) accumulator order
     Wt_ref = winograd.weight_transform(w, m)             # (T2, C, K)
     U_ref = winograd.input_transform(x, m)               # (T2, C, ntiles)
     M_ref = winograd.frequency_gemm(U_ref, Wt_ref)       # (T2, K, ntiles)
@@ -198,13 +198,24 @@ def test_three_stage_intermediates(m):
         wt_fck[f] = blk.transpose(1, 2, 0, 3).reshape(Cs * 4, Kb * 16)
     np.testing.assert_allclose(wt_fck[:, :C, :K], Wt_ref, rtol=1e-6, atol=1e-7)
     assert not wt_fck[:, C:, :].any() and not wt_fck[:, :, K:].any()
-    U = U[..., 0]
+    # U: [f4][tb][cs][lane][f%4], lane = (c%4)*16 + t%16 -> (f, c, t)
+    F4, TB, UCs = U.shape[:3]
+    u = U.reshape(F4, TB, UCs, 4, 16, 4)                     # f4, tb, cs, c%4, t%16, f%4
+    u_fct = u.transpose(0, 5, 2, 3, 1, 4).reshape(F4 * 4, UCs * 4, TB * 16)
+    assert not u_fct[T2:].any()
+    u_fct = u_fct[:T2]
     scale = np.abs(U_ref).max()
-    np.testing.assert_allclose(U[:, :C, :ntiles], U_ref, rtol=0, atol=1e-6 * scale)
-    assert not U[:, C:, :].any() and not U[:, :, ntiles:].any()
-    Mf = Mf[..., 0]
+    np.testing.assert_allclose(u_fct[:, :C, :ntiles], U_ref, rtol=0, atol=1e-6 * scale)
+    assert not u_fct[:, C:, :].any() and not u_fct[:, :, ntiles:].any()
+    # M: [f4][tb][kb][v][lane][f%4], lane = ((k%16)/4)*16 + t%16, v = k%4 -> (f, k, t)
+    F4, TB, MKb = Mf.shape[:3]
+    mm = Mf.reshape(F4, TB, MKb, 4, 4, 16, 4)                # f4, tb, kb, v, k%16/4, t%16, f%4
+    m_fkt = mm.transpose(0, 6, 2, 4, 3, 1, 5).reshape(F4 * 4, MKb * 16, TB * 16)
+    assert not m_fkt[T2:].any()
+    m_fkt = m_fkt[:T2]
     scale = np.abs(M_ref).max()
-    np.testing.assert_allclose(Mf[:, :K, :ntiles], M_ref, rtol=0, atol=1e-5 * scale)
+    np.testing.assert_allclose(m_fkt[:, :K, :ntiles], M_ref, rtol=0, atol=1e-5 * scale)
+    assert not m_fkt[:, K:, :].any() and not m_fkt[:, :, ntiles:].any()
     assert_close(y.cpu().numpy(), direct_conv(x, w), m, "three-stage end to end")
 
 
