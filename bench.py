@@ -42,7 +42,10 @@ sys.path.insert(0, ROOT)
 
 P_MFMA_F32 = 157.3e12   # MI355X dense fp32 matrix peak, FLOP/s
 B_HBM = 8.0e12          # MI355X HBM3E peak, B/s
-KERNEL_SRC = os.path.join(ROOT, "paper_1912_02165_amd", "csrc", "wino_kernels.hip")
+# the sources the fused and three-stage kernels are built from (profiles taken on
+# another version of them no longer describe the kernels)
+KERNEL_SRCS = [os.path.join(ROOT, "paper_1912_02165_amd", "csrc", f) for f in
+               ("wino_ws.h", "wino_device.h", "wino_transforms.h", "wino_kernels.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -61,8 +64,11 @@ def parse():
 
 
 def kernel_source_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(kernel, workload):

@@ -18,24 +18,30 @@ _LIB = os.path.join(_BUILD_DIR, "liboracle_direct.so")
 _lib = None
 
 
-def build(force=False):
-    """Compile ``direct_conv.c`` with gcc/OpenMP into ``oracle/_build``."""
+def build(force=False, sanitize=False, out=None):
+    """Compile ``direct_conv.c`` with gcc/OpenMP into ``oracle/_build`` (or `out`).
+    sanitize: with AddressSanitizer and UndefinedBehaviorSanitizer (for the
+    sanitizer run of the oracle pins; preload libasan when loading it)."""
     os.makedirs(_BUILD_DIR, exist_ok=True)
-    if (not force and os.path.exists(_LIB)
-            and os.path.getmtime(_LIB) >= os.path.getmtime(_SRC)):
-        return _LIB
-    tmp = _LIB + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall", "-Werror",
-           _SRC, "-o", tmp]
+    target = out or _LIB
+    if (not force and not sanitize and os.path.exists(target)
+            and os.path.getmtime(target) >= os.path.getmtime(_SRC)):
+        return target
+    tmp = target + ".tmp%d" % os.getpid()
+    san = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer",
+           "-g"] if sanitize else []
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall", "-Werror"] + san + [
+        _SRC, "-o", tmp]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, _LIB)
-    return _LIB
+    os.replace(tmp, target)
+    return target
 
 
 def _load():
     global _lib
     if _lib is None:
-        path = build()
+        # ORACLE_DIRECT_LIB selects another build (the sanitizer run's)
+        path = os.environ.get("ORACLE_DIRECT_LIB") or build()
         lib = ctypes.CDLL(path)
         i64 = ctypes.c_int64
         fp = ctypes.POINTER(ctypes.c_float)

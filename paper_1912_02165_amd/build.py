@@ -53,32 +53,43 @@ def fused_blockings():
             for m in re.findall(r"X\(([\d,\s]+)\)", body)]
 
 
-def build(verbose=False, jobs=None):
-    """Compile every source into LIB (always recompiles)."""
+# Host-side address and undefined-behaviour sanitizers (device code is never
+# built with them): for the CPU-only sanitizer run of the host tests, which loads
+# the library with the sanitizer runtime preloaded.
+HOST_SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-g"]
+
+
+def build(verbose=False, jobs=None, sanitize=False, out=None):
+    """Compile every source into LIB, or into `out` (always recompiles).
+    sanitize: instrument the host code with ASan and UBSan (the runtime is not
+    linked in; preload it when loading the library)."""
     os.makedirs(OBJDIR, exist_ok=True)
     cc = hipcc()
+    lib_path = out or LIB
+    extra = HOST_SANITIZE if sanitize else []
     tag = "%d" % os.getpid()
     units = [(src, []) for src in SOURCES]
     for m, R, kit, tb, fs, csp in fused_blockings():
         units.append((INST, [f"-DWS_M={m}", f"-DWS_TB={tb}", f"-DWS_FS={fs}", f"-DWS_CSP={csp}"]))
     objs = [os.path.join(OBJDIR, "%s.%d.%s.o" % (os.path.basename(src), i, tag))
             for i, (src, _) in enumerate(units)]
-    cmds = [[cc, f"--offload-arch={ARCH}"] + FLAGS + defs + ["-I", INCLUDE, "-I", CSRC, "-c", src, "-o", o]
+    cmds = [[cc, f"--offload-arch={ARCH}"] + FLAGS + extra + defs + ["-I", INCLUDE, "-I", CSRC, "-c", src, "-o", o]
             for (src, defs), o in zip(units, objs)]
     jobs = jobs or min(len(cmds), max(1, os.cpu_count() or 1))
-    tmp = LIB + ".tmp" + tag
+    tmp = lib_path + ".tmp" + tag
     try:
         with ThreadPoolExecutor(max_workers=jobs) as ex:
             for out in ex.map(lambda c: _run(c, verbose), cmds):
                 if verbose and out.strip():
                     print(out, flush=True)
         _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC"] + objs + ["-o", tmp], verbose)
-        os.replace(tmp, LIB)
+        os.replace(tmp, lib_path)
     finally:
         for f in objs + [tmp]:
             if os.path.exists(f):
                 os.remove(f)
-    return LIB
+    return lib_path
 
 
 if __name__ == "__main__":

@@ -776,8 +776,11 @@ SplitInfo ws_split_info(const Geometry &g, int num_cus, int csplit) {
     // dividing the stages) when at least half of the compute units would idle in
     // it otherwise.  A piece costs its workgroup a partial-output epilogue
     // (output transform, device-coherent stores, arrival count) and the last
-    // contributor a sum, which keeps P small; with four or more full rounds the
-    // imbalance is small and items stay whole.
+    // contributor a sum of coherent reloads, about 10-25 us of latency on a
+    // layer (measured: the 28x28 layer's 136-item last round split 3 ways runs in
+    // 79 us against 52.5 us whole), which keeps P small and limits splitting to
+    // mostly idle last rounds; with four or more full rounds the imbalance is
+    // small and items stay whole.
     constexpr int kMaxPieces = 4, kMaxSplitRounds = 4;
     const int tail = si.n_items - si.nfull * cus;
     if (si.nfull >= kMaxSplitRounds || tail == 0 || 2 * tail > cus) return si;

@@ -11,7 +11,8 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libwino_conv.so")
+# WINO_LIB selects another build of the same library (the sanitizer test's)
+LIB_PATH = os.environ.get("WINO_LIB") or os.path.join(HERE, "libwino_conv.so")
 
 WINO_OK, WINO_EINVAL, WINO_EUNSUPPORTED, WINO_ENOMEM, WINO_EHIP, WINO_EKERNEL = 0, -1, -2, -3, -4, -5
 WINO_ALGO_FUSED, WINO_ALGO_THREE_STAGE, WINO_ALGO_FFT = 0, 1, 2
