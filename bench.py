@@ -42,10 +42,10 @@ sys.path.insert(0, ROOT)
 
 P_MFMA_F32 = 157.3e12   # MI355X dense fp32 matrix peak, FLOP/s
 B_HBM = 8.0e12          # MI355X HBM3E peak, B/s
-# the sources the fused and three-stage kernels are built from (profiles taken on
-# another version of them no longer describe the kernels)
+# the sources the fused kernel is built from (its counters, taken on another
+# version of them, no longer describe it)
 KERNEL_SRCS = [os.path.join(ROOT, "paper_1912_02165_amd", "csrc", f) for f in
-               ("wino_ws.h", "wino_device.h", "wino_transforms.h", "wino_kernels.hip")]
+               ("wino_ws.h", "wino_device.h", "wino_transforms.h", "wino_fused_inst.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 

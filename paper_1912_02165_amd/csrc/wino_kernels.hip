@@ -72,18 +72,28 @@ __global__ void __launch_bounds__(256) weight_transform_kernel(const float *__re
 // TB = tiles_p / 16, Cs = ceil(C/4), Kb = Kb_alloc; channels, output channels and
 // tiles past the problem hold zeros.
 
+// Workgroup b of a 1-D grid of n runs on XCD b % 8; the index returned numbers the
+// workgroups so that each XCD takes one contiguous range of them.
+__device__ __forceinline__ int xcd_contiguous_block(int b, int n) {
+    const int xcd = b % 8, per = n / 8, extra = n % 8;
+    return xcd * per + (xcd < extra ? xcd : extra) + b / 8;
+}
+
 // Stage 1: the workgroup's 256 threads are 16 tiles x 16 channels (the producer
 // mapping of the fused kernel: lane%16 = tile, so the row-vector loader's DPP halo
 // exchange applies); each transforms its tile and stores one float4 per four
-// frequencies.
+// frequencies.  Workgroups are numbered tile block fastest within a channel group
+// and XCD-contiguously, so the input rows shared by vertically adjacent tiles
+// (the two overlap rows of the windows) are read from HBM once and then from L2.
 template <int M, bool VX>
 __global__ void __launch_bounds__(256) input_transform_kernel(const float *__restrict__ x,
                                                               floatx4 *__restrict__ U, Geometry g) {
     constexpr int T2 = (M + 2) * (M + 2);
     const int tid = threadIdx.x, lane = tid & 63;
     const int tr = tid & 15, cl = tid >> 4;
-    const int tb = blockIdx.x, c = blockIdx.y * 16 + cl;
     const int TB = g.tiles_p / 16;
+    const int lb = xcd_contiguous_block(blockIdx.x, gridDim.x);
+    const int tb = lb % TB, c = (lb / TB) * 16 + cl;
     if (c >= g.Cs * 4) return;  // past the last 4-channel step
     const TileIdx ti = decode_tile(g, tb * 16 + tr);
     const long long HW = (long long)g.H * g.W;
@@ -126,10 +136,7 @@ __global__ void __launch_bounds__(256) frequency_gemm_kernel(const floatx4 *__re
     constexpr int Q = freq_quads<M>();
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int TB = g.tiles_p / 16, TG = TB / 4, KG = g.Kb_alloc / 4;
-    const int nblk = gridDim.x;
-    // XCD-contiguous logical block index
-    const int xcd = blockIdx.x % 8, per = nblk / 8, extra = nblk % 8;
-    const int lb = xcd * per + (xcd < extra ? xcd : extra) + blockIdx.x / 8;
+    const int lb = xcd_contiguous_block(blockIdx.x, gridDim.x);
     const int kg = lb % KG, rest = lb / KG;
     const int tg = rest % TG, f4 = rest / TG;
     const int kb0 = kg * 4 + (wave & 1) * 2, tb0 = tg * 4 + (wave >> 1) * 2;
@@ -352,7 +359,7 @@ void describe_three_stage(const Geometry &g, char *buf, size_t len) {
 }
 
 hipError_t launch_input_transform(const Geometry &g, const float *x, float *U, hipStream_t s) {
-    dim3 block(256), grid((unsigned)(g.tiles_p / 16), (unsigned)((g.Cs * 4 + 15) / 16));
+    dim3 block(256), grid((unsigned)((long long)(g.tiles_p / 16) * ((g.Cs * 4 + 15) / 16)));
     // row-vector input loads need every row start aligned to the vector width
     const unsigned vw = (g.m == 4) ? 16u : (g.m == 5) ? 4u : 8u;
     const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
