@@ -122,27 +122,49 @@ __global__ void __launch_bounds__(256) input_transform_kernel(const float *__res
     });
 }
 
+// LDS ring depth of the three-stage product kernel, in channel steps of 8 KB.
+constexpr int kGemmSteps = 4;
+
 // Stage 2: per workgroup four frequencies (one float4 of operands) x 4 tile blocks
 // x 4 output blocks (64 tiles x 64 output channels); each of the 4 waves
 // multiplies 2 tile blocks by 2 output blocks for the 4 frequencies (16 matrix
-// products per 4-channel step from 4 operand loads of 1 KB), operands of the next
-// step loaded during the current one.  Workgroups are numbered so that the output
-// groups of one tile group are consecutive on one XCD (workgroup b runs on XCD b %
-// 8), so the tile group's U is read from HBM once and then from that XCD's L2.
+// products per 4-channel step).  A channel step's operands -- 4 KB of W' and 4 KB
+// of U, each 1 KB block already in matrix-core lane order -- are copied straight
+// from memory into an LDS ring of NS steps by the buffer unit (no registers), one
+// W' block and one U block per wave, NS - 1 steps ahead of the products; each
+// wave then reads its 2 + 2 blocks from LDS, so every operand crosses L2 once per
+// workgroup.  Workgroups are numbered so that the output groups of one tile group
+// are consecutive on one XCD (workgroup b runs on XCD b % 8), so the tile group's
+// U is read from HBM once and then from that XCD's L2.
 template <int M>
 __global__ void __launch_bounds__(256) frequency_gemm_kernel(const floatx4 *__restrict__ U,
                                                              const floatx4 *__restrict__ wt,
                                                              floatx4 *__restrict__ Mout, Geometry g) {
     constexpr int Q = freq_quads<M>();
+    constexpr int NS = kGemmSteps;
+    __shared__ floatx4 ring[NS][8][64];  // per step: W' blocks 0..3, then U blocks 0..3
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int TB = g.tiles_p / 16, TG = TB / 4, KG = g.Kb_alloc / 4;
     const int lb = xcd_contiguous_block(blockIdx.x, gridDim.x);
     const int kg = lb % KG, rest = lb / KG;
     const int tg = rest % TG, f4 = rest / TG;
-    const int kb0 = kg * 4 + (wave & 1) * 2, tb0 = tg * 4 + (wave >> 1) * 2;
     const int Cs = g.Cs;
-    const floatx4 *ap = wt + ((long long)kb0 * Cs * Q + f4) * 64 + lane;       // + (i * Cs + cs) * Q * 64
-    const floatx4 *bp = U + (((long long)f4 * TB + tb0) * Cs) * 64 + lane;     // + (j * Cs + cs) * 64
+    // The blocks this wave copies: output block 4 kg + wave of W', tile block
+    // 4 tg + wave of U; step cs at byte offset cs * Q KB (W') or cs KB (U).
+    const floatx4 *abase = wt + ((long long)(kg * 4 + wave) * Cs * Q + f4) * 64;
+    const floatx4 *bbase = U + (((long long)f4 * TB + tg * 4 + wave) * Cs) * 64;
+    const int32x4 ar = make_rsrc_uniform(reinterpret_cast<const float *>(abase),
+                                         (unsigned)(Cs - 1) * Q * 1024u + 1024u);
+    const int32x4 br = make_rsrc_uniform(reinterpret_cast<const float *>(bbase), (unsigned)Cs * 1024u);
+    const unsigned vo = (unsigned)lane * 16u;
+    // Steps past the last are clamped to it (the copies stay in bounds and every
+    // iteration issues the same number, which the vmcnt wait below relies on).
+    auto issue = [&](int st) {
+        const unsigned c = (unsigned)(st < Cs ? st : Cs - 1);
+        floatx4 *slot = ring[st % NS][0];
+        buffer_load_lds(ar, lds_ptr(slot + wave * 64), 16, vo, c * Q * 1024u, 0, 0);
+        buffer_load_lds(br, lds_ptr(slot + (4 + wave) * 64), 16, vo, c * 1024u, 0, 0);
+    };
     floatx4 acc[2][2][4];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -150,21 +172,23 @@ __global__ void __launch_bounds__(256) frequency_gemm_kernel(const floatx4 *__re
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int q = 0; q < 4; ++q) acc[i][j][q] = floatx4{0.f, 0.f, 0.f, 0.f};
-    // Operands in flight: the transformed kernels (mostly L2 hits) one step ahead,
-    // the transformed input tiles (streamed from HBM) two steps ahead, in
-    // rotating register sets; the loop is unrolled by three so every set is
-    // named statically.  Loads past the last step are clamped to it.
-    auto loada = [&](floatx4 (&a)[2], int cs) {
-        cs = cs < Cs ? cs : Cs - 1;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) a[i] = ap[((long long)i * Cs + cs) * Q * 64];
-    };
-    auto loadb = [&](floatx4 (&b)[2], int cs) {
-        cs = cs < Cs ? cs : Cs - 1;
+    for (int st = 0; st < NS - 1; ++st) issue(st);
+    const int ai = (wave & 1) * 2, bj = 4 + (wave >> 1) * 2;
+    for (int cs = 0; cs < Cs; ++cs) {
+        // This wave's copies of step cs are complete once at most the 2 (NS - 2)
+        // copies issued after them are outstanding; the barrier then makes every
+        // wave's copies of step cs visible, and tells that every wave has read
+        // step cs - 1, whose slot the next copies overwrite.
+        wait_vmcnt<2 * (NS - 2)>();
+        lds_barrier();
+        issue(cs + NS - 1);
+        const floatx4(*sl)[64] = ring[cs % NS];
+        floatx4 a[2], b[2];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) b[j] = bp[((long long)j * Cs + cs) * 64];
-    };
-    auto mul = [&](const floatx4 (&a)[2], const floatx4 (&b)[2]) {
+        for (int i = 0; i < 2; ++i) a[i] = sl[ai + i][lane];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) b[j] = sl[bj + j][lane];
 #pragma unroll
         for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -172,29 +196,9 @@ __global__ void __launch_bounds__(256) frequency_gemm_kernel(const floatx4 *__re
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[i][j][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j][q], 0, 0, 0);
-    };
-    floatx4 a0[2], a1[2], b0[2], b1[2], b2[2];
-    loadb(b0, 0);
-    loadb(b1, 1);
-    loada(a0, 0);
-    int cs = 0;
-    // step cs uses a(cs % 2), b(cs % 3); before it, step cs + 1's a and step
-    // cs + 2's b are issued
-    for (; cs + 6 <= Cs; cs += 6) {
-        loada(a1, cs + 1); loadb(b2, cs + 2); mul(a0, b0);
-        loada(a0, cs + 2); loadb(b0, cs + 3); mul(a1, b1);
-        loada(a1, cs + 3); loadb(b1, cs + 4); mul(a0, b2);
-        loada(a0, cs + 4); loadb(b2, cs + 5); mul(a1, b0);
-        loada(a1, cs + 5); loadb(b0, cs + 6); mul(a0, b1);
-        loada(a0, cs + 6); loadb(b1, cs + 7); mul(a1, b2);
     }
-    // fewer than six steps left: the sets rotate as in the loop
-    if (cs < Cs) { loada(a1, cs + 1); loadb(b2, cs + 2); mul(a0, b0); }
-    if (cs + 1 < Cs) { loada(a0, cs + 2); loadb(b0, cs + 3); mul(a1, b1); }
-    if (cs + 2 < Cs) { loada(a1, cs + 3); loadb(b1, cs + 4); mul(a0, b2); }
-    if (cs + 3 < Cs) { loada(a0, cs + 4); loadb(b2, cs + 5); mul(a1, b0); }
-    if (cs + 4 < Cs) { mul(a0, b1); }
     // M: one float4 (4 frequencies) per lane and (tile block, output block, v)
+    const int kb0 = kg * 4 + (wave & 1) * 2, tb0 = tg * 4 + (wave >> 1) * 2;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
