@@ -122,6 +122,28 @@ __global__ void __launch_bounds__(256) input_transform_kernel(const float *__res
     });
 }
 
+// Buffer-unit copy from memory straight into LDS (gfx950: `buffer_load_dwordx4 ...
+// lds`): lane l's `size` bytes at voffset + soffset of the resource land at byte
+// size * l of the wave-uniform LDS address lds.  No registers hold the data; its
+// completion is counted by vmcnt like any load.
+typedef __attribute__((address_space(3))) void *lds_void_ptr;
+__device__ void buffer_load_lds(int32x4 rsrc, lds_void_ptr lds, int size, unsigned voffset, unsigned soffset,
+                                int offset, int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+template <class P>
+__device__ __forceinline__ lds_void_ptr lds_ptr(P *p) {
+    return (lds_void_ptr)(p);
+}
+// Waits until at most N vector-memory accesses of this wave are outstanding (other
+// counters untouched).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+// Workgroup barrier with no memory wait of its own (the caller has waited for what
+// it needs); also a compiler barrier, so no LDS access moves across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 // LDS ring depth of the three-stage product kernel, in channel steps of 8 KB
 // (measured: 3 steps is 1-6 % faster than 4-6 on the deep layers, equal on the
 // others).
