@@ -18,8 +18,8 @@
  * arch is the device's architecture name (e.g. gfx950), candidates is the
  * candidate mask in hexadecimal (0x...), algo is 0 (fused), 1 (three-stage) or
  * 2 (FFT, with m = 14), R and k the fused blocking (tiles and output channels per
- * task; 0 0 for the other algorithms) and microseconds the measured time of one
- * call.
+ * task; 0 0 for the other algorithms) and microseconds the measured time per
+ * call of back-to-back calls.
  *
  * Thread safety: the wisdom table is guarded by a lock; plans are as in
  * wino_conv.h (one stream at a time).
@@ -49,8 +49,10 @@ enum {
  * current device among the candidates (a nonzero mask of WINO_TUNE_* bits with at least one
  * WINO_TUNE_M* or the WINO_TUNE_FFT bit).  If the wisdom table holds the answer it is used directly;
  * otherwise every candidate is planned and timed here: its kernels transformed
- * once, then the median of 5 calls of wino_conv_run_pretransformed after 10
- * warm-up calls, on device buffers of the layer's size that this function
+ * once, at least 20 ms of back-to-back warm-up calls of
+ * wino_conv_run_pretransformed (so that every candidate is timed at the shader
+ * clock's working frequency), then the median time per call of 5 batches of at
+ * least 1 ms of back-to-back calls, on device buffers of the layer's size that this function
  * allocates, fills with a constant and frees before returning (synchronous;
  * needs room for x, y and w beside the largest candidate's workspace).  The
  * result enters the wisdom table.  chosen_m, chosen_algo and call_us (each may

@@ -97,28 +97,46 @@ struct Buffers {
     }
 };
 
-// Median time (microseconds) of 5 calls of the plan after its kernels are
-// transformed and 10 warm-up calls (the shader clock rises over the first
-// milliseconds of work); negative status on failure.
+// GPU time (microseconds) per call of n back-to-back calls of the pretransformed
+// path, between two events on the default stream.
+int time_batch(wino_plan *p, const Buffers &b, int n, double *us) {
+    hipError_t e = hipEventRecord(b.e0, nullptr);
+    int st = WINO_OK;
+    for (int i = 0; e == hipSuccess && st == WINO_OK && i < n; ++i) st = wino_conv_run_pretransformed(p, b.x, b.y, nullptr);
+    if (st != WINO_OK) return st;
+    if (e == hipSuccess) e = hipEventRecord(b.e1, nullptr);
+    if (e == hipSuccess) e = hipEventSynchronize(b.e1);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, b.e0, b.e1);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        wino::set_error("tuning: timing failed (%s)", hipGetErrorString(e));
+        return WINO_EHIP;
+    }
+    *us = ms * 1e3 / n;
+    return WINO_OK;
+}
+
+// Time per call (microseconds) of the plan: its kernels transformed, then at
+// least kWarmUs of back-to-back calls (the shader clock needs tens of
+// milliseconds of work to reach its working frequency, so without this the first
+// candidates would be timed at a lower clock than the later ones), then the
+// median of 5 batches of back-to-back calls of at least kBatchUs each.
+constexpr double kWarmUs = 20000.0, kBatchUs = 1000.0;
 int time_plan(wino_plan *p, const Buffers &b, double *us) {
     int st = wino_conv_set_weights(p, b.w, nullptr);
-    for (int i = 0; st == WINO_OK && i < 10; ++i) st = wino_conv_run_pretransformed(p, b.x, b.y, nullptr);
-    std::vector<double> t;
-    for (int i = 0; st == WINO_OK && i < 5; ++i) {
-        hipError_t e = hipEventRecord(b.e0, nullptr);
-        if (e == hipSuccess) st = wino_conv_run_pretransformed(p, b.x, b.y, nullptr);
-        if (e == hipSuccess && st == WINO_OK) e = hipEventRecord(b.e1, nullptr);
-        if (e == hipSuccess && st == WINO_OK) e = hipEventSynchronize(b.e1);
-        float ms = 0.f;
-        if (e == hipSuccess && st == WINO_OK) e = hipEventElapsedTime(&ms, b.e0, b.e1);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            wino::set_error("tuning: timing failed (%s)", hipGetErrorString(e));
-            return WINO_EHIP;
-        }
-        t.push_back(ms * 1e3);
-    }
     if (st != WINO_OK) return st;
+    double per = 0.0, warm = 0.0;
+    int n = 4;
+    while (warm < kWarmUs) {
+        if ((st = time_batch(p, b, n, &per)) != WINO_OK) return st;
+        warm += per * n;
+        if (n < 256 && per * n < kBatchUs) n *= 2;
+    }
+    n = per > 0.0 ? (int)(kBatchUs / per) + 1 : 1;
+    std::vector<double> t(5);
+    for (double &v : t)
+        if ((st = time_batch(p, b, n, &v)) != WINO_OK) return st;
     std::sort(t.begin(), t.end());
     *us = t[t.size() / 2];
     return WINO_OK;
