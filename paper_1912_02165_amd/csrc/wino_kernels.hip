@@ -221,6 +221,9 @@ __global__ void __launch_bounds__(256) frequency_gemm_kernel(const floatx4 *__re
                 for (int j = 0; j < 2; ++j)
                     acc[i][j][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j][q], 0, 0, 0);
     }
+    // The copies issued past the last step (clamped repeats of it) must land
+    // before the workgroup ends and its LDS can be given to another workgroup.
+    wait_vmcnt<0>();
     // M: one float4 (4 frequencies) per lane and (tile block, output block, v)
     const int kb0 = kg * 4 + (wave & 1) * 2, tb0 = tg * 4 + (wave >> 1) * 2;
 #pragma unroll
