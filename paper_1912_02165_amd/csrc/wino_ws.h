@@ -773,19 +773,21 @@ SplitInfo ws_split_info(const Geometry &g, int num_cus, int csplit) {
         return si;
     }
     // Split the items of a last, partly filled round into P pieces (P <= 4,
-    // dividing the stages) when at least half of the compute units would idle in
-    // it otherwise.  A piece costs its workgroup a partial-output epilogue
-    // (output transform, device-coherent stores, arrival count) and the last
-    // contributor a sum of coherent reloads, about 10-25 us of latency on a
-    // layer (measured: the 28x28 layer's 136-item last round split 3 ways runs in
-    // 79 us against 52.5 us whole), which keeps P small and limits splitting to
-    // mostly idle last rounds; with four or more full rounds the imbalance is
-    // small and items stay whole.
-    constexpr int kMaxPieces = 4, kMaxSplitRounds = 4;
+    // dividing the stages, each piece at least 8 stages long) when at least half
+    // of the compute units would idle in it otherwise.  A piece costs its
+    // workgroup a partial-output epilogue (output transform, device-coherent
+    // stores, arrival count) and the last contributor a sum of coherent reloads,
+    // a fixed latency of several microseconds, so only long items gain
+    // (measured: the 14x14 C=K=512 layer's 64-item last round of 32-stage items
+    // split 4 ways, 344 -> 292 us at F(6); the 56x56 N=1 layer's 26 items of 4
+    // stages split 4 ways, 14.5 -> 17.9 us; the 28x28 layer's 136-item last round
+    // split 3 ways, 52.5 -> 79 us).  With four or more full rounds the imbalance
+    // is small and items stay whole.
+    constexpr int kMaxPieces = 4, kMaxSplitRounds = 4, kMinPieceStages = 8;
     const int tail = si.n_items - si.nfull * cus;
     if (si.nfull >= kMaxSplitRounds || tail == 0 || 2 * tail > cus) return si;
     int P = cus / tail < kMaxPieces ? cus / tail : kMaxPieces;
-    while (P > 1 && si.stages % P != 0) --P;
+    while (P > 1 && (si.stages % P != 0 || si.stages / P < kMinPieceStages)) --P;
     if (P < 2) return si;
     si.tail_first = si.nfull * cus;
     si.n_tail = tail;

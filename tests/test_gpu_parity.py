@@ -15,6 +15,8 @@
 * the plan's status word (bounded waits) after every call, and its plumbing.
 """
 
+import re
+
 import numpy as np
 import pytest
 import torch
@@ -33,8 +35,11 @@ SMALL = [
     (1, 5, 17, 13, 11), (3, 8, 20, 17, 23), (2, 37, 45, 29, 35), (2, 16, 33, 30, 31),
     (1, 64, 64, 20, 20), (4, 12, 40, 6, 6), (1, 130, 18, 9, 10),
     # more output channels than one group and kernels outweighing the input: items
-    # numbered tile-group fastest, most of them split into pieces
+    # numbered tile-group fastest
     (1, 32, 128, 8, 8), (2, 20, 96, 13, 6), (1, 9, 200, 5, 5),
+    # few items of 16 channel stages (the last ragged): the last round's items are
+    # split into pieces whose partial outputs are added
+    (1, 250, 40, 9, 10), (2, 256, 96, 7, 6),
 ]
 
 
@@ -219,16 +224,23 @@ def test_three_stage_intermediates(m):
     assert_close(y.cpu().numpy(), direct_conv(x, w), m, "three-stage end to end")
 
 
+def split_items(plan):
+    """Items of the plan's last round split into pieces (from its description)."""
+    found = re.search(r"split items (\d+) x (\d+) pieces", plan.describe())
+    return int(found.group(1)) if found else 0
+
+
 @pytest.mark.parametrize("m", (2, 4, 5, 6))
 def test_plan_reused_across_calls(m):
     """One plan, several calls: split items' arrival counters are back at zero after
     every call, so each call is correct and bitwise equal to the first."""
-    N, C, K, H, W = 2, 24, 80, 14, 15
+    N, C, K, H, W = 2, 256, 80, 14, 15
     x, w = workloads.random_inputs(N, C, K, H, W, seed=40 + m)
     ref = direct_conv(x, w)
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
     ys = []
     with wc.Plan(N, C, K, H, W, m) as p:
+        assert split_items(p) > 0, p.describe()
         for _ in range(3):
             y = torch.full((N, K, H, W), float("nan"), device="cuda")
             p.run(xd, wd, y)

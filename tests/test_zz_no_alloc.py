@@ -4,6 +4,8 @@ so the same bits, and within tolerance of the oracle; two calls in a row on one
 GPU share the scratch array, the second with a smaller input; layers whose scratch
 exceeds the array are refused."""
 
+import re
+
 import numpy as np
 import pytest
 import torch
@@ -34,20 +36,29 @@ def _noalloc_run(x, w, m, status):
     return y
 
 
-# pairs of calls in a row: (first shape, second, smaller, shape, m); the first of
-# each pair has split items (partial outputs and counters in the scratch), the
-# full-size 28x28 layer (N=64, C=K=128) uses 2.4 MB of transformed kernels
+# pairs of calls in a row: (first shape, second, smaller, shape, m, whether the
+# first has split items); a first call with split items keeps partial outputs and
+# counters in the scratch; the full-size 28x28 layer (N=64, C=K=128) uses 2.4 MB
+# of transformed kernels, the C=K=256 one 9.4 MB
 PAIRS = [
-    ((2, 37, 45, 29, 35), (1, 20, 24, 17, 19), 4),
-    ((1, 64, 64, 56, 56), (1, 9, 17, 13, 11), 2),
-    ((2, 24, 80, 14, 15), (1, 5, 17, 13, 11), 6),
-    ((64, 128, 128, 28, 28), (3, 64, 64, 20, 20), 4),
+    ((1, 256, 256, 28, 28), (1, 20, 24, 17, 19), 4, True),
+    ((1, 64, 64, 56, 56), (1, 9, 17, 13, 11), 2, False),
+    ((2, 256, 64, 14, 14), (1, 5, 17, 13, 11), 6, True),
+    ((2, 250, 40, 14, 15), (1, 20, 24, 17, 19), 5, True),
+    ((64, 128, 128, 28, 28), (3, 64, 64, 20, 20), 4, False),
 ]
+
+
+def _split_items(shape, m):
+    with wc.Plan(*shape, m) as p:
+        found = re.search(r"split items (\d+) x", p.describe())
+    return int(found.group(1)) if found else 0
 
 
 @pytest.mark.parametrize("pair", PAIRS, ids=lambda p: "m%d-%s" % (p[2], "x".join(map(str, p[0]))))
 def test_noalloc_matches_run_twice(pair):
-    first, second, m = pair
+    first, second, m, split = pair
+    assert (_split_items(first, m) > 0) == split
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
     for i, shape in enumerate((first, second)):
         N, C, K, H, W = shape
