@@ -383,9 +383,11 @@ def main():
                 # every work item split into channel pieces (partial outputs added)
                 cases += [(mm, "fused", "fused_csplit%d" % P) for P in (2, 4)]
             if lay.id not in fft_done:
-                # the FFT-tile algorithm (16 x 16 tiles, m = 14), once per layer
+                # the FFT-tile algorithm (16 x 16 tiles, m = 14) and the three-stage
+                # F(7x7,3x3), once per layer
                 fft_done.add(lay.id)
                 cases.append((14, "fft", "fft"))
+                cases.append((7, "three_stage", "three_stage"))
             for m_c, algo, label in cases:
                 tuning = None
                 if label.startswith("fused_csplit"):

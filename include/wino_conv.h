@@ -10,8 +10,10 @@
  * computed as the Winograd F(m x m, 3 x 3) transformed convolution of Eq. 3,
  * y = A^T [ sum_c (G w G^T) (.) (B^T d B) ] A over overlap-add tiles of edge
  * T = m + 2 (Sec. 2.1), for m in {2, 4, 5, 6} (m = 5, T = 7, is the tile of the
- * paper's experiments, Sec. 6), or as the FFT-tile convolution of the same
- * sections with T = 16 (m = 14; Sec. 4 gives T >= 16 for FFT).
+ * paper's experiments, Sec. 6) and, with the three-stage algorithm only, m = 7
+ * (T = 9: two tiles cover a 14-pixel image side exactly), or as the FFT-tile
+ * convolution of the same sections with T = 16 (m = 14; Sec. 4 gives T >= 16 for
+ * FFT).
  *
  * Layouts: x is N x C x H x W, w is K x C x 3 x 3, y is N x K x H x W, all dense
  * row-major fp32.  x, w and y are device pointers on the plan's device.
@@ -119,8 +121,8 @@ typedef struct {
  * transformed kernels (T^2 * C * K floats rounded up to the blocking) and, when
  * the last round of work items is split across compute units, their partial
  * outputs and arrival counters (zeroed here; every call leaves them zero).
- * Returns NULL (see wino_last_error) if a size is < 1, m is not 2, 4, 5 or 6 (14
- * for WINO_ALGO_FFT, which takes no other m), a
+ * Returns NULL (see wino_last_error) if a size is < 1, m is not 2, 4, 5 or 6 (also 7
+ * for WINO_ALGO_THREE_STAGE; 14 for WINO_ALGO_FFT, which takes no other m), a
  * size overflows the 32-bit offsets the kernels use (each of x and y must be
  * below 2^31 bytes), or the allocation fails. */
 wino_plan *wino_conv_plan(int N, int C, int K, int H, int W, int m);

@@ -8,7 +8,8 @@
  * F(m x m, 3 x 3), m in {2, 4, 5, 6} (the paper's T = m + 2), the fused kernel's
  * blocking at each m -- tiles per task R and output channels per task, every
  * blocking the kernel is built for (wino_fused_blockings) -- and, optionally,
- * the algorithm (three-stage at each m, or the FFT-tile algorithm with m = 14).
+ * the algorithm (three-stage at each m and at m = 7, or the FFT-tile algorithm
+ * with m = 14).
  * A tuning result is remembered per (GPU architecture, compute units, N, C, K,
  * H, W, candidate set) in a process-wide wisdom table that can be written to and
  * read from a text file.
@@ -40,6 +41,7 @@ enum {
     WINO_TUNE_M4 = 1 << 4,
     WINO_TUNE_M5 = 1 << 5,
     WINO_TUNE_M6 = 1 << 6,
+    WINO_TUNE_M7 = 1 << 7,  /* three-stage only: needs WINO_TUNE_THREE_STAGE */
     WINO_TUNE_THREE_STAGE = 1 << 8,
     WINO_TUNE_FFT = 1 << 9  /* the FFT-tile algorithm (m = 14) */
 };

@@ -37,6 +37,11 @@ Point sets (in frequency order; infinity is always last):
                                          pairs, without 0, so that every point
                                          but infinity has its mirror)
     F(6,3): 0, 1, -1, 2, -2, 1/2, -1/2
+    F(7,3): 1, -1, 2, -2, 1/2, -1/2, 1/4, -1/4
+                                        (T = 9: eight finite points in +-p pairs,
+                                         as for F(5); of the natural next pairs
+                                         +-3, +-3/2 and +-1/4, the last keeps the
+                                         fp32 error lowest, ~4e-5 relative L2)
 """
 
 from fractions import Fraction
@@ -49,6 +54,8 @@ _POINTS = {
     5: (Fraction(1), Fraction(-1), Fraction(2), Fraction(-2), Fraction(1, 2), Fraction(-1, 2)),
     6: (Fraction(0), Fraction(1), Fraction(-1), Fraction(2), Fraction(-2),
         Fraction(1, 2), Fraction(-1, 2)),
+    7: (Fraction(1), Fraction(-1), Fraction(2), Fraction(-2), Fraction(1, 2), Fraction(-1, 2),
+        Fraction(1, 4), Fraction(-1, 4)),
 }
 
 SUPPORTED_M = tuple(sorted(_POINTS))

@@ -14,7 +14,7 @@ from .wino import (  # noqa: F401
     wino_conv_info, wino_conv_intermediate_dims, wino_conv_plan, wino_conv_plan_ex, wino_conv_run,
     wino_conv_run_noalloc, wino_conv_run_pretransformed, wino_conv_set_weights, wino_conv_status, wino_conv_workspace_bytes,
     wino_last_error, wino_fused_blockings,
-    WINO_TUNE_ALL_M, WINO_TUNE_M2, WINO_TUNE_M4, WINO_TUNE_M5, WINO_TUNE_M6, WINO_TUNE_THREE_STAGE, WINO_TUNE_FFT,
+    WINO_TUNE_ALL_M, WINO_TUNE_M2, WINO_TUNE_M4, WINO_TUNE_M5, WINO_TUNE_M6, WINO_TUNE_M7, WINO_TUNE_THREE_STAGE, WINO_TUNE_FFT,
     wino_conv_plan_params, wino_conv_plan_tuned, wino_wisdom_clear, wino_wisdom_load,
     wino_wisdom_lookup, wino_wisdom_save, wino_wisdom_size,
 )

@@ -68,8 +68,15 @@ int wino::make_geometry(int N, int C, int K, int H, int W, int m, int algo, Geom
             set_err("m=%d: the FFT algorithm uses 16 x 16 tiles, m = 14", m);
             return WINO_EINVAL;
         }
+    } else if (m == 7) {
+        if (algo != WINO_ALGO_THREE_STAGE) {
+            set_err("m=7: F(7x7,3x3) runs on the three-stage algorithm only (its 81 frequencies per tile "
+                    "and channel do not fit the fused kernel's LDS stage ring)");
+            return WINO_EUNSUPPORTED;
+        }
     } else if (m != 2 && m != 4 && m != 5 && m != 6) {
-        set_err("m=%d: only F(2x2,3x3), F(4x4,3x3), F(5x5,3x3) and F(6x6,3x3) are supported", m);
+        set_err("m=%d: only F(2x2,3x3), F(4x4,3x3), F(5x5,3x3), F(6x6,3x3) and (three-stage) "
+                "F(7x7,3x3) are supported", m);
         return WINO_EINVAL;
     }
     const long long T = m + 2, TH = (H + m - 1) / m, TW = (W + m - 1) / m;

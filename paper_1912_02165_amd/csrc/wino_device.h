@@ -324,33 +324,40 @@ struct RowTile {
     }
 };
 
-// Store one m x m output tile that lies wholly inside the image through a buffer
-// resource over y: the tile's first element at byte offset voff (per lane) + soff
-// (uniform), rows rowb bytes apart (uniform), so the per-row and per-channel
-// steps are scalar adds.  STREAM: streaming (non-temporal) cache policy.
+// Store one row of m output floats through a buffer resource over y: the row's
+// first element at byte offset voff (per lane) + so (uniform).  STREAM: streaming
+// (non-temporal) cache policy.
+template <int M, bool STREAM>
+__device__ __forceinline__ void store_row_buf(int32x4 yrs, unsigned voff, unsigned so, const float *r) {
+    constexpr int kAux = STREAM ? kStream : 0;
+    if constexpr (M == 4) {
+        buffer_store_f32x4(floatx4{r[0], r[1], r[2], r[3]}, yrs, voff, so, kAux);
+    } else if constexpr (M == 5) {  // 4-byte aligned vector store + one float
+        buffer_store_f32x4(floatx4{r[0], r[1], r[2], r[3]}, yrs, voff, so, kAux);
+        buffer_store_f32(r[4], yrs, voff + 16u, so, kAux);
+    } else if constexpr (M == 7) {  // 4-byte aligned: 4 + 2 + 1 floats
+        buffer_store_f32x4(floatx4{r[0], r[1], r[2], r[3]}, yrs, voff, so, kAux);
+        buffer_store_f32x2(floatx2{r[4], r[5]}, yrs, voff + 16u, so, kAux);
+        buffer_store_f32(r[6], yrs, voff + 24u, so, kAux);
+    } else {
+#pragma unroll
+        for (int jj = 0; jj < M; jj += 2) buffer_store_f32x2(floatx2{r[jj], r[jj + 1]}, yrs, voff + 4u * jj, so, kAux);
+    }
+}
+
+// Store one m x m output tile that lies wholly inside the image: its first element
+// at byte offset voff (per lane) + soff (uniform), rows rowb bytes apart (uniform),
+// so the per-row and per-channel steps are scalar adds.
 template <int M, bool STREAM>
 __device__ __forceinline__ void store_rows_buf(int32x4 yrs, unsigned voff, unsigned soff, unsigned rowb,
                                                const float *yy) {
-    constexpr int kAux = STREAM ? kStream : 0;
 #pragma unroll
-    for (int i = 0; i < M; ++i) {
-        const unsigned so = soff + (unsigned)i * rowb;
-        if constexpr (M == 4) {
-            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, kAux);
-        } else if constexpr (M == 5) {  // 4-byte aligned vector store + one float
-            buffer_store_f32x4(floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]}, yrs, voff, so, kAux);
-            buffer_store_f32(yy[i * M + 4], yrs, voff + 16u, so, kAux);
-        } else {
-#pragma unroll
-            for (int jj = 0; jj < M; jj += 2)
-                buffer_store_f32x2(floatx2{yy[i * M + jj], yy[i * M + jj + 1]}, yrs, voff + 4u * jj, so, kAux);
-        }
-    }
+    for (int i = 0; i < M; ++i) store_row_buf<M, STREAM>(yrs, voff, soff + (unsigned)i * rowb, yy + i * M);
 }
 
 // Store one m x m output tile of plane yp (clipped to H x W).  vec: rows may be
 // written with m-float vector stores (16-byte aligned for m = 4, 8-byte for m = 2, 6;
-// m = 5 always stores element by element here).
+// odd m always stores element by element here).
 template <int M>
 __device__ __forceinline__ void store_tile(float *__restrict__ yp, const float *yy, int h0, int w0,
                                            const Geometry &g, bool vec) {
@@ -359,11 +366,11 @@ __device__ __forceinline__ void store_tile(float *__restrict__ yp, const float *
         const int h = h0 + i;
         if (h >= g.H) break;
         float *row = yp + (long long)h * g.W + w0;
-        if (M != 5 && vec && w0 + M <= g.W) {
+        if (M % 2 == 0 && vec && w0 + M <= g.W) {
             if constexpr (M == 4) {
                 *reinterpret_cast<floatx4 *>(row) =
                     floatx4{yy[i * M], yy[i * M + 1], yy[i * M + 2], yy[i * M + 3]};
-            } else if constexpr (M != 5) {
+            } else if constexpr (M % 2 == 0) {
                 #pragma unroll
                 for (int jj = 0; jj < M; jj += 2)
                     *reinterpret_cast<floatx2 *>(row + jj) = floatx2{yy[i * M + jj], yy[i * M + jj + 1]};

@@ -85,6 +85,59 @@ __device__ __forceinline__ int xcd_contiguous_block(int b, int n) {
 // frequencies.  Workgroups are numbered tile block fastest within a channel group
 // and XCD-contiguously, so the input rows shared by vertically adjacent tiles
 // (the two overlap rows of the windows) are read from HBM once and then from L2.
+// Input tile of F(7x7,3x3) (T = 9, too wide for the row-vector loader's halo
+// exchange within 16 lanes): per row the lane's own 7 columns as 4-byte-aligned
+// vector loads (4 + 2 + 1 floats) and its two halo columns as single loads; rows
+// and halo columns outside the image read as zero through the buffer range check,
+// own columns past W (the last tile of a row) are cleared.
+template <int M>
+struct WideRowTile {
+    static constexpr int T = M + 2;
+    static_assert(M == 7, "loader of the 9 x 9 input tiles");
+    unsigned roff[T];
+    unsigned own, left, right, ownok;
+
+    __device__ __forceinline__ void init(const Geometry &g, const TileIdx &t, int lane_c) {
+        const unsigned base = (unsigned)(((long long)t.n * g.C + lane_c) * g.H * g.W) * 4u;
+#pragma unroll
+        for (int a = 0; a < T; ++a) {
+            const int h = t.ty * M - 1 + a;
+            roff[a] = (t.ok && h >= 0 && h < g.H) ? base + (unsigned)(h * g.W) * 4u : kOutside;
+        }
+        own = (unsigned)(t.tx * M) * 4u;
+        left = t.tx > 0 ? own - 4u : kOutside;
+        right = t.tx * M + M < g.W ? own + 4u * M : kOutside;
+        ownok = 0u;
+#pragma unroll
+        for (int j = 0; j < M; ++j)
+            if (t.tx * M + j < g.W) ownok |= 1u << j;
+    }
+
+    __device__ __forceinline__ void load(int32x4 r, float *d) const {
+#pragma unroll
+        for (int a = 0; a < T; ++a) {
+            const unsigned ro = roff[a];
+            const floatx4 q4 = buffer_load_f32x4(r, __builtin_elementwise_add_sat(ro, own), 0, 0);
+            const floatx2 q2 = buffer_load_f32x2(r, __builtin_elementwise_add_sat(ro, own + 16u), 0, 0);
+            const float q1 = buffer_load_f32(r, __builtin_elementwise_add_sat(ro, own + 24u), 0, 0);
+            d[a * T] = buffer_load_f32(r, __builtin_elementwise_add_sat(ro, left), 0, 0);
+            d[a * T + T - 1] = buffer_load_f32(r, __builtin_elementwise_add_sat(ro, right), 0, 0);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) d[a * T + 1 + j] = q4[j];
+            d[a * T + 5] = q2[0];
+            d[a * T + 6] = q2[1];
+            d[a * T + 7] = q1;
+        }
+        if (ownok != (1u << M) - 1u) {
+#pragma unroll
+            for (int a = 0; a < T; ++a)
+#pragma unroll
+                for (int j = 0; j < M; ++j)
+                    if (!((ownok >> j) & 1u)) d[a * T + 1 + j] = 0.0f;
+        }
+    }
+};
+
 template <int M, bool VX>
 __global__ void __launch_bounds__(256) input_transform_kernel(const float *__restrict__ x,
                                                               floatx4 *__restrict__ U, Geometry g) {
@@ -99,7 +152,11 @@ __global__ void __launch_bounds__(256) input_transform_kernel(const float *__res
     const long long HW = (long long)g.H * g.W;
     const int32x4 rs = make_rsrc(x, (unsigned)((long long)g.N * g.C * HW * 4));
     float d[T2];
-    if constexpr (VX) {
+    if constexpr (VX && M == 7) {
+        WideRowTile<M> ld;
+        ld.init(g, ti, c);
+        ld.load(rs, d);
+    } else if constexpr (VX) {
         RowTile<M> ld;
         TileIdx rf, rl;
         row_edges<1>(g, tb * 16, tr, rf, rl);
@@ -261,6 +318,28 @@ __global__ void __launch_bounds__(256) output_transform_kernel(const floatx4 *__
     float yy[M * M];
     output_tile_transform<M>(mm, yy);
     (void)T2;
+    if constexpr (M % 2 == 1) {
+        // odd m: rows of tiles whose m columns lie inside the image are stored as
+        // 4-byte-aligned vector pieces (y is below 2^31 bytes), rows below the
+        // image skipped, the rows of tiles cut by the right edge element by element
+        const int h0 = ti.ty * M, w0 = ti.tx * M;
+        const bool fullw = w0 + M <= g.W;
+        const int32x4 yrs = make_rsrc(y, (unsigned)((long long)g.N * g.K * g.H * g.W * 4));
+        const unsigned vb = (unsigned)(((((long long)ti.n * g.K + k) * g.H + h0) * g.W + w0) * 4);
+        float *yp = y + ((long long)ti.n * g.K + k) * g.H * g.W;
+#pragma unroll
+        for (int i = 0; i < M; ++i) {
+            if (h0 + i >= g.H) break;
+            if (fullw) {
+                store_row_buf<M, false>(yrs, vb, (unsigned)i * (unsigned)g.W * 4u, yy + i * M);
+            } else {
+#pragma unroll
+                for (int jj = 0; jj < M; ++jj)
+                    if (w0 + jj < g.W) yp[(long long)(h0 + i) * g.W + w0 + jj] = yy[i * M + jj];
+            }
+        }
+        return;
+    }
     const bool vec = (M == 4) ? (g.W % 4 == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0)
                               : (g.W % 2 == 0 && (reinterpret_cast<uintptr_t>(y) & 7) == 0);
     store_tile<M>(y + ((long long)ti.n * g.K + k) * g.H * g.W, yy, ti.ty * M, ti.tx * M, g, vec);
@@ -269,12 +348,16 @@ __global__ void __launch_bounds__(256) output_transform_kernel(const floatx4 *__
 // ---------------------------------------------------------------------------
 // Launchers.
 
+// Tile sizes of the kernel transform and the three-stage kernels: the fused
+// kernel's and F(7x7,3x3) (T = 9: its 21 float4s of frequencies per tile and
+// channel exceed the fused kernel's LDS stage ring).
 #define WINO_DISPATCH_M(m, CALL)          \
     switch (m) {                          \
         case 2: { constexpr int MM = 2; CALL; } break; \
         case 4: { constexpr int MM = 4; CALL; } break; \
         case 5: { constexpr int MM = 5; CALL; } break; \
         case 6: { constexpr int MM = 6; CALL; } break; \
+        case 7: { constexpr int MM = 7; CALL; } break; \
         default: return hipErrorInvalidValue; \
     }
 
@@ -392,7 +475,8 @@ void describe_three_stage(const Geometry &g, char *buf, size_t len) {
 hipError_t launch_input_transform(const Geometry &g, const float *x, float *U, hipStream_t s) {
     dim3 block(256), grid((unsigned)((long long)(g.tiles_p / 16) * ((g.Cs * 4 + 15) / 16)));
     // row-vector input loads need every row start aligned to the vector width
-    const unsigned vw = (g.m == 4) ? 16u : (g.m == 5) ? 4u : 8u;
+    // (m = 5, 7: 4-byte-aligned vector loads)
+    const unsigned vw = (g.m == 4) ? 16u : (g.m == 5 || g.m == 7) ? 4u : 8u;
     const bool vx = (reinterpret_cast<uintptr_t>(x) % vw == 0) && ((unsigned)g.W * 4u) % vw == 0;
     floatx4 *u4 = reinterpret_cast<floatx4 *>(U);
     if (vx) {

@@ -11,7 +11,7 @@
 //               (infinity row: coefficients of prod_l (x - p_l)).
 // Points, in frequency order: F(2): 0, 1, -1; F(4): 0, +-1, +-2;
 // F(5): +-1, +-2, +-1/2 (no 0: T = 7 has an even number of finite points);
-// F(6): 0, +-1, +-2, +-1/2.
+// F(6): 0, +-1, +-2, +-1/2; F(7): +-1, +-2, +-1/2, +-1/4 (T = 9, no 0).
 //
 // Because the finite points are (+p, -p) pairs (after 0 for even T), the B^T rows
 // of a pair are one polynomial at x and -x: they agree on even coefficients and
@@ -54,9 +54,10 @@ constexpr bool operator==(Q a, Q b) { return a.n == b.n && a.d == b.d; }
 constexpr float to_float(Q a) { return (float)((double)a.n / (double)a.d); }
 
 constexpr Q point(int m, int j) {
-    // 0, 1, -1, 2, -2, 1/2, -1/2: the first m + 1 for even m, without 0 for odd m
-    constexpr long long num[7] = {0, 1, -1, 2, -2, 1, -1};
-    constexpr long long den[7] = {1, 1, 1, 1, 1, 2, 2};
+    // 0, 1, -1, 2, -2, 1/2, -1/2, 1/4, -1/4: the first m + 1 for even m, without 0
+    // for odd m
+    constexpr long long num[9] = {0, 1, -1, 2, -2, 1, -1, 1, -1};
+    constexpr long long den[9] = {1, 1, 1, 1, 1, 2, 2, 4, 4};
     const int i = (m % 2 == 1) ? j + 1 : j;
     return mkq(num[i], den[i]);
 }
@@ -135,7 +136,7 @@ constexpr bool pair_structure_holds() {
     return (T - 1 - pair0<M>()) % 2 == 0;  // every finite point but 0 is paired
 }
 static_assert(pair_structure_holds<2>() && pair_structure_holds<4>() && pair_structure_holds<5>() &&
-                  pair_structure_holds<6>(),
+                  pair_structure_holds<6>() && pair_structure_holds<7>(),
               "B^T rows / A^T columns of +-p points must pair up");
 
 // acc (op)= c * v with a compile-time coefficient; `first` starts the sum.

@@ -27,14 +27,21 @@ struct Choice {
 std::mutex g_mu;
 std::map<Key, Choice> g_table;
 
-constexpr unsigned kMBits = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M5 | WINO_TUNE_M6;
+// Tile sizes with fused blockings; F(7x7,3x3) runs three-stage only.
+constexpr unsigned kFusedMBits = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M5 | WINO_TUNE_M6;
+constexpr unsigned kMBits = kFusedMBits | WINO_TUNE_M7;
 constexpr unsigned kAllBits = kMBits | WINO_TUNE_THREE_STAGE | WINO_TUNE_FFT;
 
-bool mask_ok(unsigned c) { return (c & ~kAllBits) == 0 && (c & (kMBits | WINO_TUNE_FFT)) != 0; }
+// A mask is valid when it names at least one candidate: a fused tile size, the
+// FFT-tile algorithm, or m = 7 together with the three-stage algorithm.
+bool mask_ok(unsigned c) {
+    if ((c & ~kAllBits) != 0) return false;
+    return (c & (kFusedMBits | WINO_TUNE_FFT)) != 0 || ((c & WINO_TUNE_M7) && (c & WINO_TUNE_THREE_STAGE));
+}
 
 bool choice_ok(unsigned c, int m, int algo, int R, int kit) {
     if (algo == WINO_ALGO_FFT) return m == 14 && (c & WINO_TUNE_FFT) != 0 && R == 0 && kit == 0;
-    if (m != 2 && m != 4 && m != 5 && m != 6) return false;
+    if (m != 2 && m != 4 && m != 5 && m != 6 && m != 7) return false;
     if (!(c & (1u << m))) return false;
     if (algo == WINO_ALGO_THREE_STAGE) return (c & WINO_TUNE_THREE_STAGE) != 0 && R == 0 && kit == 0;
     return algo == WINO_ALGO_FUSED && wino::fused_blocking_built(m, R, kit);
@@ -151,7 +158,8 @@ wino_plan *wino_conv_plan_tuned(int N, int C, int K, int H, int W, unsigned cand
         return nullptr;
     }
     if (!mask_ok(candidates)) {
-        wino::set_error("candidate mask 0x%x: needs a WINO_TUNE_M* or WINO_TUNE_FFT bit and no other bits",
+        wino::set_error("candidate mask 0x%x: needs a WINO_TUNE_M2/4/5/6 or WINO_TUNE_FFT bit, or WINO_TUNE_M7 "
+                        "with WINO_TUNE_THREE_STAGE, and no other bits",
                         candidates);
         return nullptr;
     }
@@ -169,7 +177,7 @@ wino_plan *wino_conv_plan_tuned(int N, int C, int K, int H, int W, unsigned cand
         // candidates: per tile size every built fused blocking, the three-stage
         // algorithm if asked for, and the FFT-tile algorithm if asked for
         std::vector<Choice> cands;
-        for (int m : {2, 4, 5, 6}) {
+        for (int m : {2, 4, 5, 6, 7}) {
             if (!(candidates & (1u << m))) continue;
             for (const wino::FusedBlocking &b : wino::kFusedBlockings)
                 if (b.m == m) cands.push_back(Choice{m, WINO_ALGO_FUSED, b.R, b.kit, 0.0});

@@ -57,9 +57,10 @@ SIGNATURES = {
 }
 
 WINO_TUNE_M2, WINO_TUNE_M4, WINO_TUNE_M5, WINO_TUNE_M6 = 1 << 2, 1 << 4, 1 << 5, 1 << 6
+WINO_TUNE_M7 = 1 << 7  # three-stage only: with WINO_TUNE_THREE_STAGE
 WINO_TUNE_THREE_STAGE = 1 << 8
 WINO_TUNE_FFT = 1 << 9
-WINO_TUNE_ALL_M = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M5 | WINO_TUNE_M6
+WINO_TUNE_ALL_M = WINO_TUNE_M2 | WINO_TUNE_M4 | WINO_TUNE_M5 | WINO_TUNE_M6 | WINO_TUNE_M7
 
 WINO_MAX_CHANNEL_SPLITS = 64
 

@@ -5,6 +5,9 @@ element error normalised by the largest reference magnitude):
     F(2x2,3x3): rel_l2 <= 1e-5;  F(4x4,3x3), F(6x6,3x3): rel_l2 <= 1e-4;
     F(5x5,3x3) (not among the stated tolerances; its tile lies between F(4) and
     F(6), so it takes theirs): rel_l2 <= 1e-4;
+    F(7x7,3x3) (three-stage only; not among the stated tolerances): its transforms
+    on the points +-1, +-2, +-1/2, +-1/4 are less well conditioned, about 4e-5
+    relative L2 in fp32 over random tiles, so it takes F(4)-F(6)'s rel_l2 <= 1e-4;
     FFT tiles (16 x 16, m = 14; not among the stated tolerances): rel_l2 <= 1e-5.
     The error of an fp32 radix-2 FFT grows with the number of butterfly levels,
     about eps * log2(n) relative: 8 levels forward and 8 inverse on 16 x 16
@@ -16,7 +19,7 @@ The reference is the fp64 oracle; the GPU computes in fp32.
 
 import numpy as np
 
-REL_L2 = {2: 1e-5, 4: 1e-4, 5: 1e-4, 6: 1e-4, 14: 1e-5}
+REL_L2 = {2: 1e-5, 4: 1e-4, 5: 1e-4, 6: 1e-4, 7: 1e-4, 14: 1e-5}
 MAX_ERR = 1e-3
 
 

@@ -62,9 +62,18 @@ def test_bad_sizes(lib, args):
     assert "sizes must be >= 1" in msg
 
 
-@pytest.mark.parametrize("m", [0, 1, 3, 7, 8])
+@pytest.mark.parametrize("m", [0, 1, 3, 8])
 def test_bad_m(lib, m):
     assert "only F(2x2" in _plan_fails(lib, 1, 4, 4, 8, 8, m, wino.WINO_ALGO_FUSED, None)
+
+
+def test_m7_is_three_stage_only(lib):
+    """F(7x7,3x3) is refused by the fused algorithm (before any HIP call) and by the
+    no-allocation entry point, which runs the fused kernel."""
+    assert "three-stage algorithm only" in _plan_fails(lib, 1, 4, 4, 8, 8, 7, wino.WINO_ALGO_FUSED, None)
+    assert "m = 14" in _plan_fails(lib, 1, 4, 4, 8, 8, 7, wino.WINO_ALGO_FFT, None)
+    assert lib.wino_conv_run_noalloc(1, 4, 4, 8, 8, 7, None, None, None, None, None) == wino.WINO_EUNSUPPORTED
+    assert "three-stage algorithm only" in wc.wino_last_error()
 
 
 @pytest.mark.parametrize("m", [2, 4, 6, 13, 16])
@@ -201,6 +210,7 @@ gfx950 256 32 64 64 224 224 0x54 4 0 16 64 417.900
 gfx950 256 64 512 512 14 14 0x154 6 1 0 0 12.500
 gfx950 256 64 128 128 28 28 0x210 14 2 0 0 321.000
 gfx950 256 64 128 128 28 28 0x14 4 0 16 32 57.000
+gfx950 256 64 512 512 14 14 0x1f4 7 1 0 0 140.000
 """
 
 
@@ -210,11 +220,12 @@ def test_wisdom_roundtrip(lib, tmp_path):
     src = tmp_path / "in.txt"
     src.write_text(WISDOM)
     wc.wino_wisdom_load(str(src))
-    assert wc.wino_wisdom_size() == 4
+    assert wc.wino_wisdom_size() == 5
     assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (4, 0, 16, 64)
     assert wc.wino_wisdom_lookup("gfx950", 256, 64, 128, 128, 28, 28, 0x210) == (14, 2, 0, 0)
     assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1, 0, 0)
     assert wc.wino_wisdom_lookup("gfx950", 256, 64, 128, 128, 28, 28, 0x14) == (4, 0, 16, 32)
+    assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x1f4) == (7, 1, 0, 0)
     # every key field matters
     assert wc.wino_wisdom_lookup("gfx942", 256, 32, 64, 64, 224, 224, 0x54) is None
     assert wc.wino_wisdom_lookup("gfx950", 304, 32, 64, 64, 224, 224, 0x54) is None
@@ -223,7 +234,7 @@ def test_wisdom_roundtrip(lib, tmp_path):
     wc.wino_wisdom_save(str(out))
     wc.wino_wisdom_clear()
     wc.wino_wisdom_load(str(out))
-    assert wc.wino_wisdom_size() == 4
+    assert wc.wino_wisdom_size() == 5
     assert wc.wino_wisdom_lookup("gfx950", 256, 64, 512, 512, 14, 14, 0x154) == (6, 1, 0, 0)
     lines = [l for l in out.read_text().splitlines() if not l.startswith("#")]
     assert sorted(lines) == sorted(l for l in WISDOM.splitlines() if not l.startswith("#"))
@@ -231,7 +242,7 @@ def test_wisdom_roundtrip(lib, tmp_path):
     upd = tmp_path / "upd.txt"
     upd.write_text("gfx950 256 32 64 64 224 224 0x54 2 0 32 32 500\n")
     wc.wino_wisdom_load(str(upd))
-    assert wc.wino_wisdom_size() == 4
+    assert wc.wino_wisdom_size() == 5
     assert wc.wino_wisdom_lookup("gfx950", 256, 32, 64, 64, 224, 224, 0x54) == (2, 0, 32, 32)
     wc.wino_wisdom_clear()
 
@@ -246,6 +257,8 @@ def test_wisdom_roundtrip(lib, tmp_path):
     "gfx950 256 32 64 64 224 224 0x154 4 1 16 64 1.0",        # three-stage with a blocking
     "gfx950 256 32 64 64 224 224 0x54 4 0 32 64 1.0",         # blocking not built for m = 4
     "gfx950 256 32 64 64 224 224 0x54 6 0 16 64 1.0",         # blocking not built for m = 6
+    "gfx950 256 32 64 64 224 224 0x1d4 7 0 16 32 1.0",        # m = 7 is three-stage only
+    "gfx950 256 32 64 64 224 224 0x154 7 1 0 0 1.0",          # m = 7 not a candidate
     "gfx950 256 32 64 64 224 224 0x2 2 0 32 64 1.0",          # mask without a tile-size bit
     "gfx950 256 32 64 64 224 224 0x10 14 2 0 0 1.0",          # FFT not a candidate
     "gfx950 256 32 64 64 224 224 0x210 4 2 0 0 1.0",          # FFT with m other than 14
@@ -262,7 +275,7 @@ def test_wisdom_rejects_malformed_and_keeps_table(lib, tmp_path, line):
     bad.write_text("gfx950 256 1 1 1 1 1 0x4 2 0 32 64 1.0\n" + line + "\n")
     with pytest.raises(wc.WinoError, match=r"bad.txt:2: malformed"):
         wc.wino_wisdom_load(str(bad))
-    assert wc.wino_wisdom_size() == 4          # nothing of the bad file was merged
+    assert wc.wino_wisdom_size() == 5          # nothing of the bad file was merged
     assert wc.wino_wisdom_lookup("gfx950", 256, 1, 1, 1, 1, 1, 0x4) is None
     wc.wino_wisdom_clear()
 
@@ -274,7 +287,8 @@ def test_wisdom_file_errors(lib, tmp_path):
         wc.wino_wisdom_save(str(tmp_path / "no_such_dir" / "w.txt"))
 
 
-@pytest.mark.parametrize("mask", [0, wc.WINO_TUNE_THREE_STAGE, 1 << 3, wc.WINO_TUNE_M4 | (1 << 10)])
+@pytest.mark.parametrize("mask", [0, wc.WINO_TUNE_THREE_STAGE, 1 << 3, wc.WINO_TUNE_M4 | (1 << 10),
+                                  wc.WINO_TUNE_M7])
 def test_plan_tuned_bad_mask(lib, mask):
     assert not lib.wino_conv_plan_tuned(1, 4, 4, 8, 8, mask, None, None, None)
     assert "candidate mask" in wc.wino_last_error()

@@ -70,6 +70,17 @@ def test_small_shapes(algo, m, shape):
     assert_close(y, direct_conv(x, w), m, f"{algo} F({m}) {shape}")
 
 
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: "x".join(map(str, s)))
+def test_small_shapes_f7_three_stage(shape):
+    """F(7x7,3x3), three-stage only (T = 9: tiles wider than the row-vector loader
+    and the fused kernel's stage ring take)."""
+    N, C, K, H, W = shape
+    x, w = workloads.random_inputs(N, C, K, H, W, seed=sum(shape) + 7)
+    print(f"\n[gpu] small three_stage m=7 shape={shape}", flush=True)
+    y = run_gpu(x, w, 7, "three_stage").cpu().numpy()
+    assert_close(y, direct_conv(x, w), 7, f"three_stage F(7) {shape}")
+
+
 BLOCKINGS = wc.wino_fused_blockings()
 BLOCKING_SHAPES = [(1, 1, 1, 1, 1), (1, 3, 5, 7, 9), (2, 37, 45, 29, 35), (2, 16, 33, 30, 31),
                    (1, 130, 18, 9, 10), (1, 32, 128, 8, 8), (3, 8, 20, 17, 23), (1, 64, 64, 20, 20)]
@@ -87,8 +98,7 @@ def test_every_blocking_small(blocking, shape):
     assert_close(y, direct_conv(x, w), m, f"F({m}) R={R} Kit={kit} {shape}")
 
 
-@pytest.mark.parametrize("algo", ALGOS)
-@pytest.mark.parametrize("m", (2, 4, 5))
+@pytest.mark.parametrize("algo,m", [(a, m) for a in ALGOS for m in (2, 4, 5)] + [("three_stage", 7)])
 def test_layer1_full(algo, m):
     layer = workloads.LAYER_BY_ID[1]
     x, w = workloads.layer_inputs(layer)
@@ -161,7 +171,12 @@ def test_full_layers_fused(case):
     print(f"rel_l2={rel:.3e} max={mx:.3e} (whole output)")
 
 
-@pytest.mark.parametrize("case", [c for c in FULL_CASES if c[2] is None], ids=_case_id)
+# the three-stage path also at F(7) (every configured image side is a multiple of 7)
+THREE_STAGE_FULL = [c for c in FULL_CASES if c[2] is None] + [
+    (layer, 7, None) for layer in workloads.LAYERS if layer.id != 1]
+
+
+@pytest.mark.parametrize("case", THREE_STAGE_FULL, ids=_case_id)
 def test_full_layers_three_stage(case):
     layer, m, _ = case
     x, w, ref = layer_ref(layer)
@@ -171,7 +186,7 @@ def test_full_layers_three_stage(case):
     print(f"rel_l2={rel:.3e} max={mx:.3e} (whole output)")
 
 
-@pytest.mark.parametrize("m", (2, 4, 5, 6))
+@pytest.mark.parametrize("m", (2, 4, 5, 6, 7))
 def test_three_stage_intermediates(m):
     """Each unfused stage against the fp64 CPU Winograd's matching intermediate."""
     from oracle import winograd
@@ -273,8 +288,7 @@ def test_guard_regions_untouched(algo):
     assert_close(y.cpu().numpy(), direct_conv(x, w), 4, "guarded")
 
 
-@pytest.mark.parametrize("algo", ALGOS)
-@pytest.mark.parametrize("m", (2, 4, 5, 6))
+@pytest.mark.parametrize("algo,m", [(a, m) for a in ALGOS for m in (2, 4, 5, 6)] + [("three_stage", 7)])
 def test_pretransformed_matches_run(algo, m):
     """Kernels transformed ahead (set_weights) then run_pretransformed: the same bits
     as run, and within tolerance of the oracle."""
@@ -396,7 +410,8 @@ def _device_key():
 
 @pytest.mark.parametrize("mask", [wc.WINO_TUNE_ALL_M | wc.WINO_TUNE_THREE_STAGE, wc.WINO_TUNE_M4,
                                   wc.WINO_TUNE_M2 | wc.WINO_TUNE_M6, wc.WINO_TUNE_FFT,
-                                  wc.WINO_TUNE_M6 | wc.WINO_TUNE_FFT])
+                                  wc.WINO_TUNE_M6 | wc.WINO_TUNE_FFT,
+                                  wc.WINO_TUNE_M7 | wc.WINO_TUNE_THREE_STAGE])
 def test_plan_tuned(mask, tmp_path):
     """The tuned plan is one of the candidates, matches the oracle at its m, and is
     remembered: the second request, and one after a save / clear / load of the
@@ -514,7 +529,7 @@ def _nan_mask(N, K, H, W, m, nan_pixels):
     return mask
 
 
-NAN_CASES = [(m, algo) for m in (2, 4, 5, 6) for algo in ALGOS] + [(14, "fft")]
+NAN_CASES = [(m, algo) for m in (2, 4, 5, 6) for algo in ALGOS] + [(7, "three_stage"), (14, "fft")]
 
 
 @pytest.mark.parametrize("case", NAN_CASES, ids=lambda c: f"m{c[0]}-{c[1]}")

@@ -40,7 +40,7 @@ def _shapes(seed, count):
 
 
 CASES = ([(s, m, "fused") for m in (2, 4, 5, 6) for s in _shapes(100 + m, 6)]
-         + [(s, m, "three_stage") for m in (2, 4, 6) for s in _shapes(200 + m, 3)]
+         + [(s, m, "three_stage") for m in (2, 4, 6, 7) for s in _shapes(200 + m, 3)]
          + [(s, 14, "fft") for s in _shapes(314, 6)])
 
 
