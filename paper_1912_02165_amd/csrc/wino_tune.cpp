@@ -135,7 +135,7 @@ int time_plan(wino_plan *p, const Buffers &b, double *us) {
     if (st != WINO_OK) return st;
     double per = 0.0, warm = 0.0;
     int n = 4;
-    while (warm < kWarmUs) {
+    for (int it = 0; warm < kWarmUs && it < 1000; ++it) {  // bounded even if a batch times as 0
         if ((st = time_batch(p, b, n, &per)) != WINO_OK) return st;
         warm += per * n;
         if (n < 256 && per * n < kBatchUs) n *= 2;
