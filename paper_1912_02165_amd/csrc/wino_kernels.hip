@@ -79,12 +79,6 @@ __device__ __forceinline__ int xcd_contiguous_block(int b, int n) {
     return xcd * per + (xcd < extra ? xcd : extra) + b / 8;
 }
 
-// Stage 1: the workgroup's 256 threads are 16 tiles x 16 channels (the producer
-// mapping of the fused kernel: lane%16 = tile, so the row-vector loader's DPP halo
-// exchange applies); each transforms its tile and stores one float4 per four
-// frequencies.  Workgroups are numbered tile block fastest within a channel group
-// and XCD-contiguously, so the input rows shared by vertically adjacent tiles
-// (the two overlap rows of the windows) are read from HBM once and then from L2.
 // Input tile of F(7x7,3x3) (T = 9, too wide for the row-vector loader's halo
 // exchange within 16 lanes): per row the lane's own 7 columns as 4-byte-aligned
 // vector loads (4 + 2 + 1 floats) and its two halo columns as single loads; rows
@@ -138,6 +132,12 @@ struct WideRowTile {
     }
 };
 
+// Stage 1: the workgroup's 256 threads are 16 tiles x 16 channels (the producer
+// mapping of the fused kernel: lane%16 = tile, so the row-vector loader's DPP halo
+// exchange applies); each transforms its tile and stores one float4 per four
+// frequencies.  Workgroups are numbered tile block fastest within a channel group
+// and XCD-contiguously, so the input rows shared by vertically adjacent tiles
+// (the two overlap rows of the windows) are read from HBM once and then from L2.
 template <int M, bool VX>
 __global__ void __launch_bounds__(256) input_transform_kernel(const float *__restrict__ x,
                                                               floatx4 *__restrict__ U, Geometry g) {
