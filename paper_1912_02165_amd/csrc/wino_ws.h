@@ -653,8 +653,11 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
         // round r: issue the loads of stage r+PD, wait until buffer r % NSLOT is
         // drained, finish and transform stage r into it, and count it filled.
         // PD = 2 (three rotating register sets) keeps two stages of input loads in
-        // flight where registers allow (m <= 4), else PD = 1.
-        constexpr int PD = (M <= 4) ? 2 : 1;
+        // flight where registers allow (m = 4), else PD = 1; F(2)'s 16-float tiles
+        // allow PD = 4, so that the loads of a 64-channel item are all in flight
+        // at once (measured on the 56x56 N=1 layer: 8.4 -> 7.9 us; larger F(2)
+        // layers within 1 %).
+        constexpr int PD = (M == 2) ? 4 : (M <= 4) ? 2 : 1;
         // The loads of round r + PD are issued unconditionally (past the last stage
         // they address tiles outside every image: no memory access), so that the
         // wait for a stage's data never has to cover loads issued after it.
@@ -692,7 +695,7 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
                 round(r + 1, d1, f1, d0, f0);
             }
             if (r < nrounds) round(r, d0, f0, d1, f1);
-        } else {
+        } else if constexpr (PD == 2) {
             float d0[T2], d1[T2], d2[T2];
             unsigned f0 = 0, f1 = 0, f2 = 0;
             load_stage(d0, f0);
@@ -704,6 +707,21 @@ __global__ void __launch_bounds__(512) fused_ws_kernel(const float *__restrict__
             }
             if (r < nrounds) round(r, d0, f0, d2, f2);
             if (r + 1 < nrounds) round(r + 1, d1, f1, d0, f0);
+        } else {
+            // PD + 1 register sets rotating over the rounds (round r transforms set
+            // r % (PD + 1) and loads into the set of round r + PD), the loop
+            // unrolled by PD + 1 so that every set is named statically
+            float d[PD + 1][T2];
+            unsigned f[PD + 1] = {};
+#pragma unroll
+            for (int k = 0; k < PD; ++k) load_stage(d[k], f[k]);
+            for (; r + PD < nrounds; r += PD + 1) {
+#pragma unroll
+                for (int k = 0; k <= PD; ++k) round(r + k, d[k], f[k], d[(k + PD) % (PD + 1)], f[(k + PD) % (PD + 1)]);
+            }
+#pragma unroll
+            for (int k = 0; k < PD; ++k)
+                if (r + k < nrounds) round(r + k, d[k], f[k], d[(k + PD) % (PD + 1)], f[(k + PD) % (PD + 1)]);
         }
         return;
     }
