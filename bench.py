@@ -11,8 +11,9 @@ fp32 matrix-core roofline (transform-domain flops 2*T^2*tiles*C*K over the
 kernel's average duration, timed with HIP events on the stream it runs on), the
 three-stage variant's step time on the same layer, a per-layer table of every
 configured (layer, m) pair ("layers": fused and three-stage call and kernel
-times, matrix-core and HBM fractions of the kernels), and the CPU oracle timed
-on the host cores.  Before the W warm-up steps of every measurement, the step
+times, matrix-core and HBM fractions of the kernels), per layer the tile size,
+algorithm and blocking a per-layer tuning picks, timed the same way
+("tuned_layers"), and the CPU oracle timed on the host cores.  Before the W warm-up steps of every measurement, the step
 runs untimed for about 150 ms ("settle_ms") so that the shader clock has reached
 its steady level (it ramps up over the first tens of milliseconds of load).
 
@@ -26,7 +27,8 @@ each fused blocking the library is built for at the layer's tile sizes (algo
 "fused_R<r>_K<k>"), and on layers with C >= 128 the fused kernel with every work
 item split into 2 and 4 channel pieces (algo "fused_csplitP"); and per layer the
 FFT-tile algorithm (algo "fft", 16 x 16 tiles; its "transform-domain" rate counts
-the real flops of its complex products); and for the launch-bound 56x56 layer at
+the real flops of its complex products) and the three-stage F(7x7,3x3); and for the
+launch-bound 56x56 layer at
 F(2) one call captured in a HIP graph and replayed (algo "fused_graph").
 """
 
@@ -261,6 +263,37 @@ def layer_table(steps=20, warmup=10):
     return rows
 
 
+def tuned_table(steps=20, warmup=10):
+    """Per configured layer, the tile size, algorithm and blocking the per-layer
+    tuning picks (`wino_conv_plan_tuned` over every built fused blocking at F(2),
+    F(4), F(5), F(6) and the three-stage pipeline at those and F(7)), timed like
+    the pairs of `layer_table`."""
+    import torch
+    import paper_1912_02165_amd as wc
+    from paper_1912_02165_amd import workloads
+    rows = []
+    for lay in workloads.LAYERS:
+        xn, wn = workloads.layer_inputs(lay)
+        xa, wa = torch.from_numpy(xn).cuda(), torch.from_numpy(wn).cuda()
+        del xn, wn
+        tp = wc.Plan.tuned(lay.N, lay.C, lay.K, lay.H, lay.W, wc.WINO_TUNE_ALL_M | wc.WINO_TUNE_THREE_STAGE)
+        m, algo = tp.m, tp.algo
+        _, _, R, kit = tp.params()
+        tp.close()
+        tuning = {"tiles_per_wg": R, "k_per_wg": kit} if algo == "fused" else None
+        r = time_pair(lay, m, algo, steps, warmup, xa, wa, tuning=tuning)
+        ms = r["body_ms"] * 1e-3
+        row = {"workload": lay.tag(m), "m": m, "algo": algo, "tiles_per_wg": R, "k_per_wg": kit,
+               "ms_per_call": r["ms_per_step"], "kernel_ms": r["body_ms"],
+               "eff_tflops": r["direct_flops"] / (r["ms_per_step"] * 1e-3) / 1e12,
+               "eff_tflops_kernel": r["direct_flops"] / ms / 1e12,
+               "mfma_frac": r["tdomain_flops"] / ms / P_MFMA_F32, "kernel": r["kernel"]}
+        rows.append(row)
+        print(json.dumps(row), file=sys.stderr, flush=True)
+        del xa, wa
+    return rows
+
+
 def host_cpu():
     """(nproc, CPU model name) of the host."""
     model = ""
@@ -312,6 +345,7 @@ def main():
     from paper_1912_02165_amd import workloads
 
     layers = None if args.no_layers else layer_table()
+    tuned = None if args.no_layers else tuned_table()
     layer = workloads.LAYER_BY_ID[args.layer]
     m = args.m
     x_np, w_np = workloads.layer_inputs(layer)
@@ -353,6 +387,7 @@ def main():
         "cpu_baseline": None,
         "settle_ms": SETTLE_MS,
         "layers": layers,
+        "tuned_layers": tuned,
     }
     if not args.no_cpu:
         rec["cpu_baseline"] = cpu_baseline(layer)
