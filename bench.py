@@ -89,6 +89,9 @@ def measured_traffic(kernel, workload):
 
 
 SETTLE_MS = 150.0
+# Back-to-back timings cover at least this much GPU time (at most MAX_TIMED_CALLS calls).
+MIN_TIMED_MS = 3.0
+MAX_TIMED_CALLS = 4096
 
 
 def settle(call, ms=SETTLE_MS):
@@ -126,9 +129,13 @@ def rep_times(p, x, w, y, steps, stream, scratch=None):
     return sorted(times)[len(times) // 2]
 
 
-def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False, tuning=None):
+def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False, tuning=None, exact=False):
     """Time `steps` steps; returns dict with ms_per_step and the transform-domain
     kernel's average duration (ms) measured between events on the same stream.
+    Every back-to-back timing covers at least MIN_TIMED_MS of GPU time (more calls
+    than `steps` for small layers, so that the first dispatch's latency does not
+    weigh on the mean), except the whole steps when `exact` is set: those are then
+    exactly `steps` calls.
     per_call: also the median time of single calls, warm and cold (after a 512 MB
     scratch write that evicts L2 and the 256 MB Infinity Cache)."""
     import torch
@@ -141,28 +148,37 @@ def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False, tuning=None):
         for _ in range(warmup):
             p.run(x, w, y)
         torch.cuda.synchronize()
-        # whole steps
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        # Back-to-back calls between two events (per-call events would add a
+        # dispatch gap to every call, several microseconds against the smallest
+        # layers' kernels): `steps` calls, repeated with more calls if they took
+        # less than MIN_TIMED_MS (unless `exact`); returns ms per call.  Each
+        # timing is queued behind `pre` untimed calls of the same kind with no
+        # host synchronisation between, so that the shader clock, which falls
+        # within a millisecond or so of idling and takes tens of milliseconds to
+        # rise again, is where the previous phase left it.
+        def back_to_back(call, exact_count=False, pre=0):
+            def timed(n):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                for _ in range(pre):
+                    call()
+                a.record(stream)
+                for _ in range(n):
+                    call()
+                b.record(stream)
+                torch.cuda.synchronize()
+                return a.elapsed_time(b)
+            ms = timed(steps)
+            if exact_count or ms >= MIN_TIMED_MS:
+                return ms / steps
+            n = min(MAX_TIMED_CALLS, max(steps, int(MIN_TIMED_MS / max(ms / steps, 1e-4)) + 1))
+            return timed(n) / n
+        # whole steps, then the two phases of a step timed apart: the
+        # transform-domain kernels on the pretransformed kernels (right after the
+        # steps, behind a few of their calls), then the kernel transform
         torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(steps):
-            p.run(x, w, y)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms_step = e0.elapsed_time(e1) / steps
-        # the same two phases with an event between them: kernel transform, then the rest
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-                torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-        torch.cuda.synchronize()
-        for a, b, c in evs:
-            a.record(stream)
-            p.set_weights(w)
-            b.record(stream)
-            p.run_pretransformed(x, y)
-            c.record(stream)
-        torch.cuda.synchronize()
-        wt_ms = sum(a.elapsed_time(b) for a, b, _ in evs) / steps
-        body_ms = sum(b.elapsed_time(c) for _, b, c in evs) / steps
+        ms_step = back_to_back(lambda: p.run(x, w, y), exact)
+        body_ms = back_to_back(lambda: p.run_pretransformed(x, y), pre=max(4, warmup))
+        wt_ms = back_to_back(lambda: p.set_weights(w))
         nt, dflops, tflops = p.info()
         p.status()
         res = {"ms_per_step": ms_step, "weight_transform_ms": wt_ms, "body_ms": body_ms,
@@ -352,8 +368,8 @@ def main():
     x = torch.from_numpy(x_np).cuda()
     w = torch.from_numpy(w_np).cuda()
 
-    fused = time_pair(layer, m, "fused", args.steps, args.warmup, x, w)
-    three = time_pair(layer, m, "three_stage", args.steps, args.warmup, x, w)
+    fused = time_pair(layer, m, "fused", args.steps, args.warmup, x, w, exact=True)
+    three = time_pair(layer, m, "three_stage", args.steps, args.warmup, x, w, exact=True)
 
     kernel_ms = fused["body_ms"]
     achieved = fused["tdomain_flops"] / (kernel_ms * 1e-3)
@@ -377,8 +393,8 @@ def main():
         "roofline": {"bound": "mfma", "achieved": achieved / 1e12, "peak": P_MFMA_F32 / 1e12,
                      "unit": "TFLOP/s", "frac": achieved / P_MFMA_F32, "traffic": traffic,
                      "kernel": fused["kernel"], "kernel_ms": kernel_ms,
-                     "kernel_ms_timing": "HIP events around run_pretransformed on its stream, "
-                                         "mean of the timed steps"},
+                     "kernel_ms_timing": "HIP events around `steps` back-to-back run_pretransformed "
+                                         "calls on its stream, mean per call"},
         "tdomain_tflops_per_step": fused["tdomain_flops"] / (fused["ms_per_step"] * 1e-3) / 1e12,
         "weight_transform_ms": fused["weight_transform_ms"],
         "three_stage": {"ms_per_step": three["ms_per_step"],
