@@ -129,6 +129,23 @@ def rep_times(p, x, w, y, steps, stream, scratch=None):
     return sorted(times)[len(times) // 2]
 
 
+def per_call_ms(timed, steps, exact=False):
+    """Mean ms per call of back-to-back calls between two events (per-call events
+    would add a dispatch gap to every call, several microseconds against the
+    smallest layers' kernels).  `timed(n)` queues n calls between two events and
+    returns the elapsed ms; it is called for `steps` calls and, unless `exact`,
+    once more with enough calls to cover MIN_TIMED_MS (at most MAX_TIMED_CALLS)
+    when those took less.  Each window is queued behind untimed calls of the same
+    kind with no host synchronisation between, so that the shader clock, which
+    falls within a millisecond or so of idling and takes tens of milliseconds to
+    rise again, is where the previous phase left it."""
+    ms = timed(steps)
+    if exact or ms >= MIN_TIMED_MS:
+        return ms / steps
+    n = min(MAX_TIMED_CALLS, max(steps, int(MIN_TIMED_MS / max(ms / steps, 1e-4)) + 1))
+    return timed(n) / n
+
+
 def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False, tuning=None, exact=False):
     """Time `steps` steps; returns dict with ms_per_step and the transform-domain
     kernel's average duration (ms) measured between events on the same stream.
@@ -148,30 +165,22 @@ def time_pair(layer, m, algo, steps, warmup, x, w, per_call=False, tuning=None, 
         for _ in range(warmup):
             p.run(x, w, y)
         torch.cuda.synchronize()
-        # Back-to-back calls between two events (per-call events would add a
-        # dispatch gap to every call, several microseconds against the smallest
-        # layers' kernels): `steps` calls, repeated with more calls if they took
-        # less than MIN_TIMED_MS (unless `exact`); returns ms per call.  Each
-        # timing is queued behind `pre` untimed calls of the same kind with no
-        # host synchronisation between, so that the shader clock, which falls
-        # within a millisecond or so of idling and takes tens of milliseconds to
-        # rise again, is where the previous phase left it.
+
+        # n back-to-back calls between two events, behind `pre` untimed ones
+        def window(call, n, pre):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            for _ in range(pre):
+                call()
+            a.record(stream)
+            for _ in range(n):
+                call()
+            b.record(stream)
+            torch.cuda.synchronize()
+            return a.elapsed_time(b)
+
         def back_to_back(call, exact_count=False, pre=0):
-            def timed(n):
-                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                for _ in range(pre):
-                    call()
-                a.record(stream)
-                for _ in range(n):
-                    call()
-                b.record(stream)
-                torch.cuda.synchronize()
-                return a.elapsed_time(b)
-            ms = timed(steps)
-            if exact_count or ms >= MIN_TIMED_MS:
-                return ms / steps
-            n = min(MAX_TIMED_CALLS, max(steps, int(MIN_TIMED_MS / max(ms / steps, 1e-4)) + 1))
-            return timed(n) / n
+            return per_call_ms(lambda n: window(call, n, pre), steps, exact_count)
+
         # whole steps, then the two phases of a step timed apart: the
         # transform-domain kernels on the pretransformed kernels (right after the
         # steps, behind a few of their calls), then the kernel transform

@@ -1,7 +1,8 @@
 """Host-side checks of bench.py (no GPU): it refuses more than one GPU with a
 message before touching a device, its measured-traffic lookup only accepts
-entries taken on the current kernel source, and every workload of the table
-exists."""
+entries taken on the current kernel source, and its per-call timing takes
+exactly the requested calls for the timed steps and a longer window only where
+asked."""
 
 import json
 import os
@@ -37,3 +38,36 @@ def test_traffic_entries_match_the_kernel_source():
     else:
         assert got is None
     assert bench.measured_traffic("fused", "no such workload") is None
+
+
+class _FakeTimer:
+    """Stands in for a window of n back-to-back calls of `ms_each` milliseconds."""
+
+    def __init__(self, ms_each):
+        self.ms_each = ms_each
+        self.windows = []
+
+    def __call__(self, n):
+        self.windows.append(n)
+        return n * self.ms_each
+
+
+def test_timed_steps_are_exactly_the_requested_calls():
+    for ms_each in (0.008, 0.37):
+        t = _FakeTimer(ms_each)
+        assert abs(bench.per_call_ms(t, 100, exact=True) - ms_each) < 1e-12
+        assert t.windows == [100]
+
+
+def test_short_windows_are_lengthened_to_the_minimum_time():
+    t = _FakeTimer(0.008)  # 20 calls of 8 us: 0.16 ms, below MIN_TIMED_MS
+    assert abs(bench.per_call_ms(t, 20) - 0.008) < 1e-12
+    assert t.windows[0] == 20 and len(t.windows) == 2
+    assert t.windows[1] * 0.008 >= bench.MIN_TIMED_MS
+    assert t.windows[1] <= bench.MAX_TIMED_CALLS
+    long = _FakeTimer(0.37)  # 20 calls of 370 us already cover the minimum
+    bench.per_call_ms(long, 20)
+    assert long.windows == [20]
+    tiny = _FakeTimer(1e-7)  # never more than MAX_TIMED_CALLS
+    bench.per_call_ms(tiny, 20)
+    assert tiny.windows[1] == bench.MAX_TIMED_CALLS
