@@ -3,6 +3,8 @@ run path allocates nothing and issues no memset, and the split path's arrival
 counters are left at zero by every call.  Each replay, with eager work and
 synchronisations between replays, must equal the eager result bit for bit."""
 
+import re
+
 import pytest
 import torch
 
@@ -12,7 +14,9 @@ from paper_1912_02165_amd import workloads
 pytestmark = pytest.mark.gpu
 
 CASES = [
-    # (N, C, K, H, W, m, algo): the 56x56 layer splits its last round of items
+    # (N, C, K, H, W, m, algo); the C=256 28x28 layer splits its last round of
+    # items into channel pieces (partial outputs, arrival counters)
+    ((1, 256, 256, 28, 28), 4, "fused"),
     ((1, 64, 64, 56, 56), 4, "fused"),
     ((1, 64, 64, 56, 56), 2, "fused"),
     ((2, 37, 45, 29, 35), 6, "fused"),
@@ -28,6 +32,8 @@ def test_graph_replay_matches_eager(case):
     print(f"\n[gpu] graph replay {case}", flush=True)
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
     with wc.Plan(N, C, K, H, W, m, algo) as p:
+        if C == 256:
+            assert re.search(r"split items [1-9]", p.describe()), p.describe()
         ref = torch.empty((N, K, H, W), device="cuda")
         p.run(xd, wd, ref)
         torch.cuda.synchronize()
