@@ -4,7 +4,8 @@ An output y (and, separately, an input x) of 99 % of that limit is run and
 checked against the oracle on three output planes: the first, one in the
 middle and the last, whose stores sit at the largest offsets of y; the layers
 read the whole of x for each of them.  The planes are computed once per shape
-and shared by the tile sizes and algorithms."""
+and shared by the tile sizes and algorithms (Winograd F(2)-F(7) and the FFT
+tiles)."""
 
 import numpy as np
 import pytest
@@ -20,7 +21,8 @@ Y_LIMIT = (1, 16, 128, 2040, 2040)   # y: 128 * 2040^2 * 4 = 2,130,739,200 bytes
 X_LIMIT = (1, 128, 16, 2040, 2040)   # x: the same bytes on the input side
 CASES = [(Y_LIMIT, 2, "fused"), (Y_LIMIT, 4, "fused"), (Y_LIMIT, 5, "fused"), (Y_LIMIT, 6, "fused"),
          (Y_LIMIT, 4, "three_stage"), (Y_LIMIT, 7, "three_stage"),
-         (X_LIMIT, 4, "fused"), (X_LIMIT, 6, "fused"), (X_LIMIT, 4, "three_stage")]
+         (Y_LIMIT, 14, "fft"),
+         (X_LIMIT, 4, "fused"), (X_LIMIT, 6, "fused"), (X_LIMIT, 4, "three_stage"), (X_LIMIT, 14, "fft")]
 
 _cache = {}
 
