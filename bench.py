@@ -8,14 +8,16 @@ seeded synthetic tensors already resident in device memory.
 The metric is the effective rate, direct-convolution flops (2*N*C*K*H*W*9) per
 second.  The JSON line also carries the fused kernel's own rate against the
 fp32 matrix-core roofline (transform-domain flops 2*T^2*tiles*C*K over the
-kernel's average duration, timed with HIP events on the stream it runs on), the
+kernel's mean duration: K back-to-back calls of it alone between two HIP events
+on the stream it runs on, queued right behind the timed steps), the
 three-stage variant's step time on the same layer, a per-layer table of every
 configured (layer, m) pair ("layers": fused and three-stage call and kernel
 times, matrix-core and HBM fractions of the kernels), per layer the tile size,
 algorithm and blocking a per-layer tuning picks, timed the same way
-("tuned_layers"), and the CPU oracle timed on the host cores.  Before the W warm-up steps of every measurement, the step
-runs untimed for about 150 ms ("settle_ms") so that the shader clock has reached
-its steady level (it ramps up over the first tens of milliseconds of load).
+("tuned_layers"), and the CPU oracle timed on the host cores.  Before the W
+warm-up steps of every measurement, the step runs untimed for about 150 ms
+("settle_ms") so that the shader clock has reached its steady level (it ramps up
+over the first tens of milliseconds of load).
 
     python bench.py [--steps K] [--warmup W] [--layer ID --m M] [--all] [--no-cpu] [--no-layers]
 
@@ -28,8 +30,8 @@ each fused blocking the library is built for at the layer's tile sizes (algo
 item split into 2 and 4 channel pieces (algo "fused_csplitP"); and per layer the
 FFT-tile algorithm (algo "fft", 16 x 16 tiles; its "transform-domain" rate counts
 the real flops of its complex products) and the three-stage F(7x7,3x3); and for the
-launch-bound 56x56 layer at
-F(2) one call captured in a HIP graph and replayed (algo "fused_graph").
+launch-bound 56x56 layer at F(2) one call captured in a HIP graph and replayed
+(algo "fused_graph").
 """
 
 import argparse
